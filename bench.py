@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Benchmark of the few-bit activation hot path on one MI355X.
+
+One step = one forward (y = f(x), classify, pack b-bit codes) plus one
+backward (unpack, grad_in = grad_out * v[idx]) over the whole tensor: every
+row of the hot path.  Default workload: GELU, 3 bits, bf16 x of shape
+[16, 2048, 8192] (268,435,456 elements) drawn as 0.99 N(0,1) + 0.01 N(0,10^2),
+grad_out ~ N(0,1), inputs resident in HBM before timing starts.
+
+Prints ONE JSON line.  `value` is the whole-step throughput in GB/s of
+algorithmic bytes: forward reads x (s bytes) and writes y (s) and codes
+(b/8); backward reads grad_out (s) and codes (b/8) and writes grad_in (s).
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--bits B]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "fwd+bwd GB/s & % HBM peak (elements/s), GELU 3-bit bf16 [16,2048,8192]"
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+
+
+def algorithmic_bytes(n: int, dtype: str, bits: int) -> float:
+    s = 4 if dtype == "f32" else 2
+    return n * (2 * s + bits / 8.0)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("paper_2202_00441_amd/csrc/fewbit.hip",):
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, bits: int, kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as fh:
+            d = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    rec = d.get("launches", {}).get(f"{workload}/b{bits}/{kernel}")
+    return rec.get("hbm_bytes") if rec else None
+
+
+def cpu_baseline(w, bits, x_np, g_np, seconds=10.0, chunk=1 << 22):
+    """The oracle, single-threaded, over consecutive chunks of the same input
+    until `seconds` of CPU time have been spent.  It uses the oracle's own
+    fitted table (tests/golden/tables.json)."""
+    import numpy as np
+    import oracle as O
+    act = {"gelu": O.GELU, "silu": O.SILU, "sigmoid": O.SIGMOID, "tanh": O.TANH}[w.act]
+    odt = {"f32": O.F32, "f16": O.F16, "bf16": O.BF16}[w.dtype]
+    with open(os.path.join(ROOT, "tests", "golden", "tables.json")) as fh:
+        spec = json.load(fh)[f"{w.name}/b{bits}"]
+    s = np.float32([float.fromhex(h) for h in spec["s"]])
+    v = np.float32([float.fromhex(h) for h in spec["v"]])
+    done, t_total, pos = 0, 0.0, 0
+    while t_total < seconds and pos < x_np.size:
+        xs = x_np[pos:pos + chunk]
+        gs = g_np[pos:pos + chunk]
+        t0 = time.perf_counter()
+        _, codes = O.fwd(act, odt, bits, s, xs)
+        O.bwd(odt, bits, v, gs, codes)
+        t_total += time.perf_counter() - t0
+        done += xs.size
+        pos += chunk
+    eps = done / t_total
+    return {
+        "value": round(eps * algorithmic_bytes(1, w.dtype, bits) * 2 / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "elements_per_s": round(eps, 1),
+        "sample": f"first {done} elements of the same workload ({done // chunk} chunks of "
+                  f"{chunk}), forward + backward, scalar C oracle in double, one thread, "
+                  f"{t_total:.1f} s",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="cfg4_gelu_bf16_lm_ffn")
+    ap.add_argument("--bits", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this path runs on one GPU; figures for more than one GPU are not "
+              "measured here (the method is pointwise and shards without communication).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as WL
+    import paper_2202_00441_amd as P
+
+    w = WL.WORKLOADS[args.workload]
+    bits = args.bits
+    assert bits in w.bits, f"{w.name} runs bits {w.bits}"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t0 = time.time()
+    x_np, g_np = WL.inputs(w)
+    print(f"[bench] generated {w.name} n={w.n} in {time.time() - t0:.1f}s", file=sys.stderr,
+          flush=True)
+    view = np.int32 if w.dtype == "f32" else np.int16
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[w.dtype]
+    x = torch.from_numpy(x_np.view(view)).to(dev).view(tdt)
+    g = torch.from_numpy(g_np.view(view)).to(dev).view(tdt)
+    y = torch.empty_like(x)
+    gin = torch.empty_like(g)
+    n = w.n
+    codes = torch.empty(P.packed_words(n, bits), dtype=torch.int32, device=dev)
+
+    table = P.fit_table(w.act, bits, P.Weight.from_spec(w.fit), w.fit["n_grid"])
+
+    def step():
+        P.fwd(table, x, y=y, codes=codes)
+        P.bwd(table, g, codes, grad_in=gin)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-kernel events on the stream the kernels are launched on
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        P.fwd(table, x, y=y, codes=codes)
+        ev[k][1].record(stream)
+        P.bwd(table, g, codes, grad_in=gin)
+        ev[k][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+
+    fwd_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(args.steps)]
+    bwd_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]
+    fwd_avg = sum(fwd_ms) / len(fwd_ms)
+    bwd_avg = sum(bwd_ms) / len(bwd_ms)
+    bytes_pass = algorithmic_bytes(n, w.dtype, bits)
+    ms_per_step = wall * 1e3 / args.steps
+    gbps = 2 * bytes_pass / (ms_per_step * 1e-3) / 1e9
+
+    # plain copy of the same element count (read s*n, write s*n): the
+    # practical streaming ceiling on this device
+    cp_dst = torch.empty_like(x)
+    for _ in range(3):
+        cp_dst.copy_(x)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(10):
+        cp_dst.copy_(x)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_ms = c0.elapsed_time(c1) / 10
+    copy_gbps = 2 * x.numel() * x.element_size() / (copy_ms * 1e-3) / 1e9
+    del cp_dst
+
+    dom = "fwd" if fwd_avg >= bwd_avg else "bwd"
+    dom_ms = fwd_avg if dom == "fwd" else bwd_avg
+    achieved = bytes_pass / (dom_ms * 1e-3) / 1e9
+    traffic = measured_traffic(w.name, bits, dom)
+
+    out = {
+        "metric": METRIC,
+        "value": round(gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded numpy draws, see workloads.py)",
+        "config": {
+            "workload": f"{w.name}: {w.act.upper()} {bits}-bit {w.dtype} {list(w.shape)}",
+            "act": w.act, "bits": bits, "shape": list(w.shape), "n": n,
+            "x": {"normal": f"N(0,{w.x_scale}^2)",
+                  "mixture": f"0.99 N(0,{w.x_scale}^2) + 0.01 N(0,{10 * w.x_scale}^2)",
+                  "uniform": f"U(-{w.x_scale},{w.x_scale})"}[w.x_dist],
+            "grad_out": f"N(0,{w.g_sigma}^2)",
+            "table": f"fewbit_fit_table {w.fit}",
+        },
+        "pct_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
+        "elements_per_s": round(2 * n / (ms_per_step * 1e-3), 1),
+        "fwd": {"ms": round(fwd_avg, 5), "GB/s": round(bytes_pass / (fwd_avg * 1e-3) / 1e9, 2),
+                "elements_per_s": round(n / (fwd_avg * 1e-3), 1),
+                "frac_peak": round(bytes_pass / (fwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
+        "bwd": {"ms": round(bwd_avg, 5), "GB/s": round(bytes_pass / (bwd_avg * 1e-3) / 1e9, 2),
+                "elements_per_s": round(n / (bwd_avg * 1e-3), 1),
+                "frac_peak": round(bytes_pass / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
+        "copy_ceiling": {"GB/s": round(copy_gbps, 2), "ms": round(copy_ms, 5),
+                         "what": "torch copy_ of x (read+write, same element count)"},
+        "roofline": {
+            "kernel": f"{dom}_kernel<{w.dtype},{bits},{w.act}>",
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "bytes_per_launch": bytes_pass,
+            "avg_launch_ms": round(dom_ms, 5),
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, bits, x_np, g_np, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

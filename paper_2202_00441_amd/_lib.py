@@ -1,0 +1,217 @@
+"""ctypes binding of libfewbit.so (the C ABI declared in include/fewbit.h).
+
+Argument marshalling only: every step of the forward and backward runs in
+the library's HIP kernels; PyTorch supplies device memory and the stream.
+There is no fallback: if the shared library is missing or fails to load,
+importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libfewbit.so")
+
+# status codes, activations, storage types, weights, flags (include/fewbit.h)
+OK, E_INVALID, E_NULL, E_ALIGN, E_DTYPE, E_BITS, E_NOMEM, E_NUMERIC, E_HIP = \
+    0, -1, -2, -3, -4, -5, -6, -7, -8
+GELU, SILU, SIGMOID, TANH = 0, 1, 2, 3
+F32, F16, BF16 = 0, 1, 2
+W_UNIFORM, W_NORMAL, W_MIXTURE = 0, 1, 2
+FLAG_SYMMETRIC = 1
+
+ACTS = {"gelu": GELU, "silu": SILU, "swish": SILU, "sigmoid": SIGMOID, "tanh": TANH}
+DTYPES = {"f32": F32, "f16": F16, "bf16": BF16}
+
+
+class FewbitError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {strerror(status)} (status {status})")
+        self.status = status
+
+
+class CWeight(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("reserved", C.c_int32), ("A", C.c_double),
+                ("B", C.c_double), ("mu", C.c_double), ("sigma", C.c_double),
+                ("p", C.c_double), ("sigma2", C.c_double)]
+
+
+class CTable(C.Structure):
+    _fields_ = [("act", C.c_int32), ("bits", C.c_int32), ("flags", C.c_int32),
+                ("reserved", C.c_int32), ("s", C.c_float * 15), ("v", C.c_float * 16),
+                ("loss", C.c_double)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2202_00441_amd.build` "
+            "(there is no CPU fallback)")
+    L = C.CDLL(LIB_PATH)
+    i32, i64, vp = C.c_int32, C.c_int64, C.c_void_p
+    L.fewbit_fit_table.restype = C.c_int
+    L.fewbit_fit_table.argtypes = [i32, i32, C.POINTER(CWeight), i64, i32, C.POINTER(CTable)]
+    L.fewbit_packed_words.restype = i64
+    L.fewbit_packed_words.argtypes = [i64, i32]
+    L.fewbit_fwd.restype = C.c_int
+    L.fewbit_fwd.argtypes = [C.POINTER(CTable), i32, vp, vp, vp, i64, vp]
+    L.fewbit_bwd.restype = C.c_int
+    L.fewbit_bwd.argtypes = [C.POINTER(CTable), i32, vp, vp, vp, i64, vp]
+    L.fewbit_strerror.restype = C.c_char_p
+    L.fewbit_strerror.argtypes = [i32]
+    return L
+
+
+lib = _load()
+
+
+def strerror(status: int) -> str:
+    return lib.fewbit_strerror(int(status)).decode()
+
+
+@dataclass(frozen=True)
+class Weight:
+    """w(x) of Eq. (3); zero outside [A, B]."""
+    kind: int
+    A: float
+    B: float
+    mu: float = 0.0
+    sigma: float = 1.0
+    p: float = 0.0
+    sigma2: float = 1.0
+
+    def c(self) -> CWeight:
+        return CWeight(self.kind, 0, self.A, self.B, self.mu, self.sigma, self.p, self.sigma2)
+
+    @staticmethod
+    def from_spec(spec: dict) -> "Weight":
+        kind = {"uniform": W_UNIFORM, "normal": W_NORMAL, "mixture": W_MIXTURE}[spec["kind"]]
+        return Weight(kind, spec["A"], spec["B"], spec.get("mu", 0.0), spec.get("sigma", 1.0),
+                      spec.get("p", 0.0), spec.get("sigma2", 1.0))
+
+
+class Table:
+    """A fitted approximation (fewbit_table): K-1 boundaries, K values."""
+
+    def __init__(self, ct: CTable):
+        self.c = ct
+
+    @property
+    def act(self) -> int:
+        return self.c.act
+
+    @property
+    def bits(self) -> int:
+        return self.c.bits
+
+    @property
+    def flags(self) -> int:
+        return self.c.flags
+
+    @property
+    def s(self) -> list:
+        return [self.c.s[i] for i in range((1 << self.bits) - 1)]
+
+    @property
+    def v(self) -> list:
+        return [self.c.v[i] for i in range(1 << self.bits)]
+
+    @property
+    def loss(self) -> float:
+        return self.c.loss
+
+    @staticmethod
+    def from_values(act: int, bits: int, s: Sequence[float], v: Sequence[float],
+                    flags: int = 0, loss: float = 0.0) -> "Table":
+        K = 1 << bits
+        if len(s) != K - 1 or len(v) != K:
+            raise ValueError("need 2^bits - 1 boundaries and 2^bits values")
+        ct = CTable()
+        ct.act, ct.bits, ct.flags, ct.reserved = act, bits, flags, 0
+        for i in range(15):
+            ct.s[i] = float(s[i]) if i < K - 1 else float("inf")
+        for i in range(16):
+            ct.v[i] = float(v[i]) if i < K else 0.0
+        ct.loss = loss
+        return Table(ct)
+
+
+def fit_table(act, bits: int, weight: Weight, n_grid: int, symmetric: bool = False) -> Table:
+    """fewbit_fit_table: the dynamic-programming fit of Sec. 3 (host)."""
+    a = ACTS[act] if isinstance(act, str) else int(act)
+    ct = CTable()
+    cw = weight.c()
+    rc = lib.fewbit_fit_table(a, int(bits), C.byref(cw), int(n_grid),
+                              FLAG_SYMMETRIC if symmetric else 0, C.byref(ct))
+    if rc != OK:
+        raise FewbitError(rc, "fewbit_fit_table")
+    return Table(ct)
+
+
+def packed_words(n: int, bits: int) -> int:
+    return int(lib.fewbit_packed_words(int(n), int(bits)))
+
+
+# ---------------------------------------------------------------- raw pointers
+def fwd_raw(table: Table, dtype: int, x: int, y: int, codes: int, n: int, stream: int) -> int:
+    return lib.fewbit_fwd(C.byref(table.c), dtype, x, y, codes, n, stream)
+
+
+def bwd_raw(table: Table, dtype: int, g: int, codes: int, gin: int, n: int, stream: int) -> int:
+    return lib.fewbit_bwd(C.byref(table.c), dtype, g, codes, gin, n, stream)
+
+
+# ---------------------------------------------------------------- torch tensors
+def _dtype_code(t) -> int:
+    import torch
+    m = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+    if t.dtype not in m:
+        raise TypeError(f"unsupported dtype {t.dtype}")
+    return m[t.dtype]
+
+
+def _stream(dev) -> int:
+    import torch
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def fwd(table: Table, x, y=None, codes=None):
+    """y = f(x) and the packed interval indices (Listing 1, forward).
+
+    x: contiguous CUDA tensor (fp32 / fp16 / bf16).  Returns (y, codes) with
+    codes a uint32-sized int32 tensor of packed_words(x.numel(), bits) words.
+    """
+    import torch
+    if not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous device tensor")
+    n = x.numel()
+    if y is None:
+        y = torch.empty_like(x)
+    if codes is None:
+        codes = torch.empty(max(packed_words(n, table.bits), 1), dtype=torch.int32,
+                            device=x.device)
+    with torch.cuda.device(x.device):
+        rc = fwd_raw(table, _dtype_code(x), x.data_ptr(), y.data_ptr(), codes.data_ptr(), n,
+                     _stream(x.device))
+    if rc != OK:
+        raise FewbitError(rc, "fewbit_fwd")
+    return y, codes
+
+
+def bwd(table: Table, grad_out, codes, grad_in=None):
+    """grad_in = grad_out * v[idx] (Eq. (1) with the approximation of f')."""
+    import torch
+    if not grad_out.is_cuda or not grad_out.is_contiguous():
+        raise ValueError("grad_out must be a contiguous device tensor")
+    n = grad_out.numel()
+    if grad_in is None:
+        grad_in = torch.empty_like(grad_out)
+    with torch.cuda.device(grad_out.device):
+        rc = bwd_raw(table, _dtype_code(grad_out), grad_out.data_ptr(), codes.data_ptr(),
+                     grad_in.data_ptr(), n, _stream(grad_out.device))
+    if rc != OK:
+        raise FewbitError(rc, "fewbit_bwd")
+    return grad_in

@@ -1,0 +1,254 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bit-exact on packed codes and grad_in; y within 2e-6 abs + 1e-5 rel (fp32)
+or 1 ulp (fp16 / bf16).  Cases: all five workloads at full size (the sizes
+the benchmark runs, in its launch configuration), the same workloads cut to
+ragged lengths, an edge-size sweep over every dtype x bits x activation,
+special values, boundaries, in-place aliasing, a second stream, canaries
+past every output, and the autograd wrapper.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as WL
+from parity import (OACT, ODT, THREADS, check_exact, check_y, download, download_codes,
+                    golden_table, run_case, upload)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2202_00441_amd as P  # noqa: E402
+
+_INPUTS = {}
+
+
+def inputs(name, limit=None):
+    key = (name, limit)
+    if key not in _INPUTS:
+        _INPUTS.clear()
+        _INPUTS[key] = WL.inputs(WL.WORKLOADS[name], limit)
+    return _INPUTS[key]
+
+
+FULL = [(name, b) for name, w in WL.WORKLOADS.items() for b in w.bits]
+
+
+@pytest.mark.parametrize("name,bits", FULL, ids=[f"{n}-b{b}" for n, b in FULL])
+def test_workload_full_size(name, bits):
+    w = WL.WORKLOADS[name]
+    x, g = inputs(name)
+    stats = run_case(f"{name}/b{bits}", w.dtype, x, g, label=f"{name} b{bits} full")
+    print(stats, flush=True)
+
+
+RAGGED = [1, 7, 511, 512, 513, 4097, 100003]
+
+
+@pytest.mark.parametrize("name,bits", FULL, ids=[f"{n}-b{b}" for n, b in FULL])
+def test_workload_ragged_prefixes(name, bits):
+    w = WL.WORKLOADS[name]
+    x, g = inputs(name, limit=200000)
+    for n in RAGGED:
+        run_case(f"{name}/b{bits}", w.dtype, x[:n].copy(), g[:n].copy(),
+                 label=f"{name} b{bits} n={n}")
+
+
+EDGE_N = [1, 2, 31, 32, 33, 63, 64, 65, 511, 512, 513, 1023, 1024, 1025, 4095, (1 << 20) + 7]
+
+
+def _synthetic_table(act, bits):
+    import oracle as O
+    key = {"gelu": "cfg1_gelu3_f32_1M/b3", "silu": "cfg3_silu2_f16_resnet/b2",
+           "sigmoid": "cfg5_sigmoid4_f32_odd/b4", "tanh": "cfg5_tanh3_f32_odd/b3"}[act]
+    spec, _ = golden_table(key)
+    if spec["bits"] == bits:
+        s = np.float32([float.fromhex(h) for h in spec["s"]])
+        v = np.float32([float.fromhex(h) for h in spec["v"]])
+    else:
+        F = O.fit(OACT[act], bits, O.uniform(-8.0, 8.0), 400)
+        s, v = F.s, F.v
+    return s, v, P.Table.from_values(P.ACTS[act], bits, s, v)
+
+
+def _run_synthetic(act, bits, dt, x_bits, g_bits, label):
+    s, v, table = _synthetic_table(act, bits)
+    n = x_bits.size
+    print(f"[edge] {label} act={act} dt={dt} bits={bits} n={n}", flush=True)
+    y_ref, c_ref = O.fwd(OACT[act], ODT[dt], bits, s, x_bits, threads=THREADS)
+    gin_ref = O.bwd(ODT[dt], bits, v, g_bits, c_ref, threads=THREADS)
+    x = upload(x_bits, dt)
+    y, codes = P.fwd(table, x)
+    gin = P.bwd(table, upload(g_bits, dt), codes)
+    torch.cuda.synchronize()
+    check_exact(download_codes(codes)[:P.packed_words(n, bits)], c_ref, f"{label} codes")
+    check_y(download(y, dt), y_ref, dt, f"{label} y")
+    check_exact(download(gin, dt), gin_ref, f"{label} grad_in")
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+def test_edge_sizes_gelu(dt, bits):
+    rng = np.random.default_rng(100 + bits)
+    for n in EDGE_N:
+        x = O.round_array(ODT[dt], rng.normal(0, 2, n))
+        g = O.round_array(ODT[dt], rng.normal(0, 1, n))
+        _run_synthetic("gelu", bits, dt, x, g, f"edge n={n}")
+
+
+@pytest.mark.parametrize("act", ["silu", "sigmoid", "tanh"])
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_edge_sizes_other_acts(act, dt):
+    rng = np.random.default_rng(7)
+    for bits in (1, 3, 4):
+        for n in (1, 33, 513, 4097):
+            x = O.round_array(ODT[dt], rng.uniform(-9, 9, n))
+            g = O.round_array(ODT[dt], rng.normal(0, 1, n))
+            _run_synthetic(act, bits, dt, x, g, f"{act} n={n}")
+
+
+def _special_values(dt, s):
+    big = {"f32": 3.0e38, "f16": 65000.0, "bf16": 3.0e38}[dt]
+    tiny = {"f32": [1e-45, 1e-40, 1.17e-38], "f16": [6e-8, 3e-6, 6.1e-5],
+            "bf16": [1e-40, 9.2e-41, 1.2e-38]}[dt]
+    vals = [0.0, -0.0, np.inf, -np.inf, np.nan, -np.nan, big, -big]
+    vals += tiny + [-t for t in tiny]
+    # every boundary, and its neighbours in the storage type
+    for b in s:
+        bb = float(b)
+        vals.append(bb)
+        vals.append(bb * (1 + 2 ** -20) if bb else 1e-30)
+        vals.append(bb * (1 - 2 ** -20) if bb else -1e-30)
+    # the GELU / SiLU tail where outputs pass through the subnormals
+    vals += list(np.linspace(-16.0, -12.0, 257)) + list(np.linspace(-110.0, -80.0, 97))
+    vals += list(np.linspace(-20.0, 20.0, 401))
+    return np.array(vals, np.float64)
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu", "sigmoid", "tanh"])
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_special_values_and_boundaries(act, dt):
+    bits = 3
+    s, v, table = _synthetic_table(act, bits)
+    xd = _special_values(dt, s)
+    x = O.round_array(ODT[dt], xd)
+    # boundary neighbours in the storage type itself
+    if dt == "f32":
+        sb = s.view(np.uint32)
+        extra = np.concatenate([sb, sb + 1, sb - 1])
+        extra = extra[(extra & 0x7F800000) != 0x7F800000]
+        x = np.concatenate([x, extra.astype(np.uint32)])
+    else:
+        hb = O.round_array(ODT[dt], s.astype(np.float64))
+        x = np.concatenate([x, hb, (hb + 1).astype(np.uint16), (hb - 1).astype(np.uint16)])
+    x = np.tile(x, 3)            # several tiles' worth, with a ragged end
+    rng = np.random.default_rng(11)
+    g = O.round_array(ODT[dt], rng.normal(0, 1, x.size))
+    _run_synthetic(act, bits, dt, x, g, f"special {act}")
+
+
+def _canary_buffers(n, dt, bits):
+    pad_e, pad_w = 256, 64
+    y_full = torch.empty(n + pad_e, dtype=torch.int32 if dt == "f32" else torch.int16,
+                         device="cuda")
+    y_full.fill_(0x5A5A)
+    c_full = torch.empty(P.packed_words(n, bits) + pad_w, dtype=torch.int32, device="cuda")
+    c_full.fill_(0x3C3C3C3C)
+    return y_full, c_full
+
+
+@pytest.mark.parametrize("dt,bits", [("bf16", 3), ("f32", 3), ("f16", 1), ("bf16", 4), ("f32", 2)])
+def test_no_write_past_the_end(dt, bits):
+    rng = np.random.default_rng(12)
+    s, v, table = _synthetic_table("gelu", bits)
+    for n in (1, 37, 511, 1025, 67109 * 3 + 1):
+        x = upload(O.round_array(ODT[dt], rng.normal(0, 2, n)), dt)
+        y_full, c_full = _canary_buffers(n, dt, bits)
+        nw = P.packed_words(n, bits)
+        from parity import torch_dtype
+        y = y_full[:n].view(torch_dtype(dt))
+        P.fwd(table, x, y=y, codes=c_full[:nw])
+        gin_full, _ = _canary_buffers(n, dt, bits)
+        P.bwd(table, x, c_full[:nw], grad_in=gin_full[:n].view(torch_dtype(dt)))
+        torch.cuda.synchronize()
+        assert bool((y_full[n:] == 0x5A5A).all()), f"y written past the end n={n}"
+        assert bool((gin_full[n:] == 0x5A5A).all()), f"grad_in written past the end n={n}"
+        assert bool((c_full[nw:] == 0x3C3C3C3C).all()), f"codes written past the end n={n}"
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_in_place(dt):
+    rng = np.random.default_rng(13)
+    n = 100000 + 3
+    s, v, table = _synthetic_table("gelu", 3)
+    xb = O.round_array(ODT[dt], rng.normal(0, 2, n))
+    gb = O.round_array(ODT[dt], rng.normal(0, 1, n))
+    y_ref, c_ref = O.fwd(O.GELU, ODT[dt], 3, s, xb, threads=THREADS)
+    gin_ref = O.bwd(ODT[dt], 3, v, gb, c_ref, threads=THREADS)
+    x = upload(xb, dt)
+    _, codes = P.fwd(table, x, y=x)                 # y == x
+    g = upload(gb, dt)
+    P.bwd(table, g, codes, grad_in=g)               # grad_in == grad_out
+    torch.cuda.synchronize()
+    check_y(download(x, dt), y_ref, dt, "in-place y")
+    check_exact(download_codes(codes)[:c_ref.size], c_ref, "in-place codes")
+    check_exact(download(g, dt), gin_ref, "in-place grad_in")
+
+
+def test_side_stream():
+    rng = np.random.default_rng(14)
+    n = 300001
+    s, v, table = _synthetic_table("gelu", 3)
+    xb = O.round_array(O.BF16, rng.normal(0, 2, n))
+    y_ref, c_ref = O.fwd(O.GELU, O.BF16, 3, s, xb, threads=THREADS)
+    x = upload(xb, "bf16")
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(st):
+        y, codes = P.fwd(table, x)
+    torch.cuda.current_stream().wait_stream(st)
+    torch.cuda.synchronize()
+    check_exact(download_codes(codes)[:c_ref.size], c_ref, "stream codes")
+    check_y(download(y, "bf16"), y_ref, "bf16", "stream y")
+
+
+def test_misaligned_pointer_is_rejected():
+    s, v, table = _synthetic_table("gelu", 3)
+    x = torch.zeros(1000, dtype=torch.bfloat16, device="cuda")
+    y = torch.zeros(1000, dtype=torch.bfloat16, device="cuda")
+    c = torch.zeros(200, dtype=torch.int32, device="cuda")
+    rc = P.fwd_raw(table, P.BF16, x.data_ptr() + 2, y.data_ptr(), c.data_ptr(), 10,
+                   torch.cuda.current_stream().cuda_stream)
+    assert rc == -3
+
+
+def test_autograd_wrapper():
+    rng = np.random.default_rng(15)
+    n = 8 * 512 * 3 + 5
+    s, v, table = _synthetic_table("gelu", 3)
+    xb = O.round_array(O.BF16, rng.normal(0, 2, n))
+    gb = O.round_array(O.BF16, rng.normal(0, 1, n))
+    x = upload(xb, "bf16").requires_grad_(True)
+    y = P.FewBitActivation.apply(x, table)
+    y.backward(upload(gb, "bf16"))
+    torch.cuda.synchronize()
+    y_ref, c_ref = O.fwd(O.GELU, O.BF16, 3, s, xb, threads=THREADS)
+    gin_ref = O.bwd(O.BF16, 3, v, gb, c_ref, threads=THREADS)
+    check_y(download(y.detach(), "bf16"), y_ref, "bf16", "autograd y")
+    check_exact(download(x.grad, "bf16"), gin_ref, "autograd grad")
+
+
+def test_module_fits_its_own_table():
+    m = P.FewBitAct("gelu", 3)
+    assert len(m.table.s) == 7 and m.table.loss > 0
+    x = torch.randn(4096 + 3, device="cuda", dtype=torch.float32, requires_grad=True)
+    y = m(x)
+    y.sum().backward()
+    torch.cuda.synchronize()
+    codes = O.fwd(O.GELU, O.F32, 3, np.float32(m.table.s),
+                  x.detach().cpu().numpy().view(np.uint32), want_idx=True)[2]
+    ref = np.float32(m.table.v)[codes]
+    assert np.array_equal(x.grad.cpu().numpy(), ref)

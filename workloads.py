@@ -81,42 +81,51 @@ WORKLOADS = {
 HEADLINE = ("cfg4_gelu_bf16_lm_ffn", 3)
 
 
-def _to_storage(z: np.ndarray, dtype: str) -> np.ndarray:
-    if dtype == "f32":
-        return z.astype(np.float32).view(np.uint32)
-    if dtype == "f16":
-        return z.astype(np.float16).view(np.uint16)
-    if dtype == "bf16":
-        import torch
-        f = torch.from_numpy(z.astype(np.float32))
-        return f.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
-    raise ValueError(dtype)
-
-
 def _storage_type(dtype: str):
     return np.uint32 if dtype == "f32" else np.uint16
 
 
 def draw(dist: str, scale: float, n: int, dtype: str, seed: int, limit: int | None = None):
-    """n (or the first `limit`) seeded draws as storage bit patterns."""
+    """n (or the first `limit`) seeded draws as storage bit patterns.
+
+    Works chunk by chunk in preallocated buffers (the values are those of
+    one draw of the whole array)."""
     m = n if limit is None else min(n, limit)
     out = np.empty(m, _storage_type(dtype))
     rng = np.random.default_rng(seed)
     rng_mask = np.random.default_rng(seed + 2000) if dist == "mixture" else None
+    cmax = min(CHUNK, max(m, 1))
+    z = np.empty(cmax)
+    u = np.empty(cmax) if dist == "mixture" else None
+    f32 = np.empty(cmax, np.float32) if dtype == "bf16" else None
     pos = 0
     while pos < m:
         c = min(CHUNK, m - pos)
+        zc = z[:c]
         if dist == "normal":
-            z = rng.standard_normal(c) * scale
+            rng.standard_normal(out=zc)
+            zc *= scale
         elif dist == "mixture":
-            z = rng.standard_normal(c) * scale
-            mask = rng_mask.random(c) < 0.01
-            z[mask] *= 10.0
+            rng.standard_normal(out=zc)
+            zc *= scale
+            rng_mask.random(out=u[:c])
+            zc[u[:c] < 0.01] *= 10.0
         elif dist == "uniform":
-            z = rng.uniform(-scale, scale, c)
+            zc[...] = rng.uniform(-scale, scale, c)
         else:
             raise ValueError(dist)
-        out[pos:pos + c] = _to_storage(z, dtype)
+        dst = out[pos:pos + c]
+        if dtype == "f32":
+            dst.view(np.float32)[...] = zc
+        elif dtype == "f16":
+            dst.view(np.float16)[...] = zc
+        elif dtype == "bf16":
+            import torch
+            f32[:c] = zc
+            torch.from_numpy(dst.view(np.int16)).view(torch.bfloat16).copy_(
+                torch.from_numpy(f32[:c]))
+        else:
+            raise ValueError(dtype)
         pos += c
     return out
 
