@@ -46,6 +46,12 @@ class CTable(C.Structure):
 
 
 def _load():
+    # torch ships its own HIP runtime (file libamdhip64.so, soname
+    # libamdhip64.so.7).  Loading torch first makes the dynamic loader reuse
+    # that runtime for libfewbit.so's libamdhip64.so.7 dependency; loading
+    # libfewbit.so first would map the system runtime and torch would then
+    # map a second one, and launches through the first would see no device.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"{LIB_PATH} is missing: build it with `python -m paper_2202_00441_amd.build` "

@@ -21,6 +21,8 @@
 
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
+#include <cstdlib>
 
 #include "../../include/fewbit.h"
 
@@ -336,6 +338,17 @@ int check_table(const fewbit_table* t) {
   return FEWBIT_OK;
 }
 
+// Status of the launch just made; with FEWBIT_DEBUG set in the environment
+// the HIP error behind FEWBIT_E_HIP is printed to stderr.
+int launch_status(const char* where) {
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) return FEWBIT_OK;
+  if (std::getenv("FEWBIT_DEBUG"))
+    std::fprintf(stderr, "fewbit: %s launch failed: %s (%s)\n", where, hipGetErrorName(e),
+                 hipGetErrorString(e));
+  return FEWBIT_E_HIP;
+}
+
 bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
 TableArgs table_args(const fewbit_table* t) {
@@ -415,12 +428,16 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   if (!x || !y || !codes) return FEWBIT_E_NULL;
   if (misaligned(x) || misaligned(y) || misaligned(codes)) return FEWBIT_E_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // the runtime's last-error slot may hold an error left by an earlier,
+  // unrelated call on this thread; clear it so the check below sees only
+  // this launch
+  (void)hipGetLastError();
   switch (dtype) {
     case FEWBIT_F32: launch_fwd_bits<FEWBIT_F32>(t, x, y, codes, n, s); break;
     case FEWBIT_F16: launch_fwd_bits<FEWBIT_F16>(t, x, y, codes, n, s); break;
     default: launch_fwd_bits<FEWBIT_BF16>(t, x, y, codes, n, s); break;
   }
-  return hipGetLastError() == hipSuccess ? FEWBIT_OK : FEWBIT_E_HIP;
+  return launch_status("fewbit_fwd");
 }
 
 extern "C" int fewbit_bwd(const fewbit_table* t, int32_t dtype, const void* grad_out,
@@ -433,12 +450,13 @@ extern "C" int fewbit_bwd(const fewbit_table* t, int32_t dtype, const void* grad
   if (!grad_out || !codes || !grad_in) return FEWBIT_E_NULL;
   if (misaligned(grad_out) || misaligned(codes) || misaligned(grad_in)) return FEWBIT_E_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();  // see fewbit_fwd
   switch (dtype) {
     case FEWBIT_F32: launch_bwd_bits<FEWBIT_F32>(t, grad_out, codes, grad_in, n, s); break;
     case FEWBIT_F16: launch_bwd_bits<FEWBIT_F16>(t, grad_out, codes, grad_in, n, s); break;
     default: launch_bwd_bits<FEWBIT_BF16>(t, grad_out, codes, grad_in, n, s); break;
   }
-  return hipGetLastError() == hipSuccess ? FEWBIT_OK : FEWBIT_E_HIP;
+  return launch_status("fewbit_bwd");
 }
 
 extern "C" const char* fewbit_strerror(int32_t status) {

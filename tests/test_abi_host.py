@@ -172,3 +172,14 @@ def test_fwd_bwd_errors_before_launch():
 def test_table_from_values_rejects_wrong_lengths():
     with pytest.raises(ValueError):
         P.Table.from_values(P.GELU, 3, [0.0] * 6, [0.0] * 8)
+
+
+def test_single_hip_runtime_in_process():
+    # one HIP runtime per process: the library must bind to torch's
+    import torch  # noqa: F401
+    paths = set()
+    with open("/proc/self/maps") as fh:
+        for line in fh:
+            if "libamdhip64" in line:
+                paths.add(os.path.realpath(line.split()[-1]))
+    assert len(paths) == 1, paths
