@@ -216,7 +216,8 @@ def main():
         "copy_ceiling": {"GB/s": round(copy_gbps, 2), "ms": round(copy_ms, 5),
                          "what": "torch copy_ of x (read+write, same element count)"},
         "roofline": {
-            "kernel": f"{dom}_kernel<{w.dtype},{bits},{w.act}>",
+            "kernel": (f"fwd{32 if w.dtype == 'f32' else 16}_kernel" if dom == "fwd" else "bwd_kernel")
+                      + f"<{w.dtype},{bits},{w.act}>",
             "bound": "hbm",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBPS,

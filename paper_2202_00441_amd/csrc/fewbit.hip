@@ -15,10 +15,24 @@
 // with quad permutes instead of atomics or shared memory, and every packed
 // word has exactly one writer.
 //
-// The table (boundaries s, values v) travels as kernel arguments, i.e. in
-// scalar registers; the backward mirrors v into LDS for per-lane lookup.
+// Streams are read and written with non-temporal 16-byte accesses (nothing
+// is reused), by a grid sized to the device's compute units so each wave
+// walks many tiles.
+//
+// Classification.  For fp16 / bf16 inputs every one of the 65536 input bit
+// patterns gets its interval index in a 64 KiB LDS table, built by each
+// workgroup from the boundaries before streaming (the index is monotone in
+// the value within a run of patterns that share sign and exponent, so the
+// table is filled run by run and checked at both ends of each 16-pattern
+// run; only runs holding a boundary, infinities or NaNs are evaluated one by
+// one).  A lookup then costs one LDS byte read instead of 2^b - 1 compares.
+// fp32 inputs compare against the boundaries held in scalar registers.
+//
+// The table travels as kernel arguments (scalar registers); the backward
+// mirrors the values into LDS for per-lane lookup.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstdio>
@@ -26,14 +40,49 @@
 
 #include "../../include/fewbit.h"
 
+// Launch-shape knobs (compile time): threads per workgroup, workgroups per
+// CU (the grid is capped at that many per compute unit and waves then walk
+// the tiles) and tiles in flight per wave, per kernel.  The fp16 / bf16
+// forward holds a 64 KiB table per workgroup, so at most 2 fit per CU.
+#ifndef FEWBIT_FWD16_THREADS
+#define FEWBIT_FWD16_THREADS 256
+#endif
+#ifndef FEWBIT_FWD16_WG_PER_CU
+#define FEWBIT_FWD16_WG_PER_CU 2
+#endif
+#ifndef FEWBIT_FWD16_UNROLL
+#define FEWBIT_FWD16_UNROLL 4
+#endif
+#ifndef FEWBIT_FWD32_THREADS
+#define FEWBIT_FWD32_THREADS 256
+#endif
+#ifndef FEWBIT_FWD32_WG_PER_CU
+#define FEWBIT_FWD32_WG_PER_CU 4
+#endif
+#ifndef FEWBIT_FWD32_UNROLL
+#define FEWBIT_FWD32_UNROLL 2
+#endif
+#ifndef FEWBIT_BWD_THREADS
+#define FEWBIT_BWD_THREADS 512
+#endif
+#ifndef FEWBIT_BWD_WG_PER_CU
+#define FEWBIT_BWD_WG_PER_CU 2
+#endif
+#ifndef FEWBIT_BWD_UNROLL
+#define FEWBIT_BWD_UNROLL 2
+#endif
+#ifndef FEWBIT_NT_LOADS
+#define FEWBIT_NT_LOADS 1             // non-temporal stream loads
+#endif
+#ifndef FEWBIT_NT_STORES
+#define FEWBIT_NT_STORES 1            // non-temporal stream stores
+#endif
+
 namespace {
 
 constexpr int kWave = 64;
 constexpr int kPerLane = 8;                 // elements per lane per tile
 constexpr int kTile = kWave * kPerLane;     // 512 elements per wave tile
-constexpr int kBlock = 256;                 // 4 waves per workgroup
-constexpr int kWavesPerBlock = kBlock / kWave;
-constexpr int64_t kMaxBlocks = 256 * 8;     // 8 resident workgroups per CU
 
 struct TableArgs {
   float s[15];
@@ -43,133 +92,200 @@ struct TableArgs {
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ inline u32x4_t ld_stream(const void* p) {
+  if constexpr (FEWBIT_NT_LOADS) return __builtin_nontemporal_load(static_cast<const u32x4_t*>(p));
+  return *static_cast<const u32x4_t*>(p);
+}
+__device__ inline void st_stream(void* p, u32x4_t v) {
+  if constexpr (FEWBIT_NT_STORES) __builtin_nontemporal_store(v, static_cast<u32x4_t*>(p));
+  else *static_cast<u32x4_t*>(p) = v;
+}
 
 // ---------------------------------------------------------------- storage
+// Half types: two elements per 32-bit word, element 2k in the low half.
 template <int DT>
-struct Storage;
+struct Half;
 
 template <>
-struct Storage<FEWBIT_F32> {
-  __device__ static void load8(const void* p, int64_t e, float (&f)[8]) {
-    const float4* q = reinterpret_cast<const float4*>(static_cast<const float*>(p) + e);
-    const float4 a = q[0], b = q[1];
-    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w;
-    f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
-  }
-  __device__ static void store8(void* p, int64_t e, const float (&f)[8]) {
-    float4* q = reinterpret_cast<float4*>(static_cast<float*>(p) + e);
-    q[0] = make_float4(f[0], f[1], f[2], f[3]);
-    q[1] = make_float4(f[4], f[5], f[6], f[7]);
-  }
-  __device__ static float load1(const void* p, int64_t e) {
-    return static_cast<const float*>(p)[e];
-  }
-  __device__ static void store1(void* p, int64_t e, float v) {
-    static_cast<float*>(p)[e] = v;
-  }
-};
-
-// bfloat16 is the upper half of a binary32: widening is a shift; narrowing
-// rounds to nearest even (v_cvt_pk_bf16_f32 on gfx950).
-template <>
-struct Storage<FEWBIT_BF16> {
+struct Half<FEWBIT_BF16> {
+  // bfloat16 is the upper half of a binary32: widening is a shift
   __device__ static float lo(uint32_t u) { return __uint_as_float(u << 16); }
   __device__ static float hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+  __device__ static float widen(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+  // round to nearest even (v_cvt_pk_bf16_f32)
   __device__ static uint32_t pack(float a, float b) {
-    const bf16x2_t h = __builtin_convertvector((f32x2_t){a, b}, bf16x2_t);
-    return __builtin_bit_cast(uint32_t, h);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
   }
-  __device__ static void load8(const void* p, int64_t e, float (&f)[8]) {
-    const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + e);
-    f[0] = lo(u.x); f[1] = hi(u.x); f[2] = lo(u.y); f[3] = hi(u.y);
-    f[4] = lo(u.z); f[5] = hi(u.z); f[6] = lo(u.w); f[7] = hi(u.w);
-  }
-  __device__ static void store8(void* p, int64_t e, const float (&f)[8]) {
-    uint4 u;
-    u.x = pack(f[0], f[1]); u.y = pack(f[2], f[3]);
-    u.z = pack(f[4], f[5]); u.w = pack(f[6], f[7]);
-    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p) + e) = u;
-  }
-  __device__ static float load1(const void* p, int64_t e) {
-    return __uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(p)[e]) << 16);
-  }
-  __device__ static void store1(void* p, int64_t e, float v) {
-    static_cast<uint16_t*>(p)[e] = static_cast<uint16_t>(pack(v, 0.0f) & 0xFFFFu);
-  }
+  __device__ static bool special_run(uint32_t p) { return (p & 0x7F80u) == 0x7F80u; }
 };
 
 template <>
-struct Storage<FEWBIT_F16> {
+struct Half<FEWBIT_F16> {
+  __device__ static float lo(uint32_t u) {
+    return static_cast<float>(__builtin_bit_cast(f16x2_t, u).x);
+  }
+  __device__ static float hi(uint32_t u) {
+    return static_cast<float>(__builtin_bit_cast(f16x2_t, u).y);
+  }
+  __device__ static float widen(uint32_t bits16) {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
+  }
   __device__ static uint32_t pack(float a, float b) {
-    const f16x2_t h = __builtin_convertvector((f32x2_t){a, b}, f16x2_t);
-    return __builtin_bit_cast(uint32_t, h);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, f16x2_t));
   }
-  __device__ static void unpack(uint32_t u, float& a, float& b) {
-    const f16x2_t h = __builtin_bit_cast(f16x2_t, u);
-    a = static_cast<float>(h.x);
-    b = static_cast<float>(h.y);
+  __device__ static bool special_run(uint32_t p) { return (p & 0x7C00u) == 0x7C00u; }
+};
+
+// element-wise access for the partial tile at the end
+template <int DT>
+struct Scalar {
+  __device__ static float load(const void* p, int64_t e) {
+    return Half<DT>::widen(static_cast<const uint16_t*>(p)[e]);
   }
-  __device__ static void load8(const void* p, int64_t e, float (&f)[8]) {
-    const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + e);
-    unpack(u.x, f[0], f[1]); unpack(u.y, f[2], f[3]);
-    unpack(u.z, f[4], f[5]); unpack(u.w, f[6], f[7]);
+  __device__ static void store(void* p, int64_t e, float v) {
+    static_cast<uint16_t*>(p)[e] = static_cast<uint16_t>(Half<DT>::pack(v, 0.0f) & 0xFFFFu);
   }
-  __device__ static void store8(void* p, int64_t e, const float (&f)[8]) {
-    uint4 u;
-    u.x = pack(f[0], f[1]); u.y = pack(f[2], f[3]);
-    u.z = pack(f[4], f[5]); u.w = pack(f[6], f[7]);
-    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p) + e) = u;
-  }
-  __device__ static float load1(const void* p, int64_t e) {
-    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<const uint16_t*>(p)[e]));
-  }
-  __device__ static void store1(void* p, int64_t e, float v) {
-    static_cast<uint16_t*>(p)[e] = static_cast<uint16_t>(pack(v, 0.0f) & 0xFFFFu);
-  }
+};
+template <>
+struct Scalar<FEWBIT_F32> {
+  __device__ static float load(const void* p, int64_t e) { return static_cast<const float*>(p)[e]; }
+  __device__ static void store(void* p, int64_t e, float v) { static_cast<float*>(p)[e] = v; }
 };
 
 // ---------------------------------------------------------------- activations
-// Each f is evaluated in fp32.  The products x*Phi(x) and x*sigmoid(x) are
-// formed as relu(x) - |x| * tail(|x|), with tail the upper tail probability
-// (Q for the normal, sigmoid(-|x|) for the logistic), so the negative side
-// keeps full relative accuracy down to the subnormal range.
-template <int ACT>
+// f evaluated in fp32 with hardware exp2 / reciprocal.  x*Phi(x) and
+// x*sigmoid(x) are formed as relu(x) - |x| * tail(|x|), tail the upper tail
+// probability, which keeps full relative accuracy on the negative side down
+// to the subnormals.
+//
+// The hardware exponential returns no subnormals (results below 2^-126 come
+// back as 0), so each exponential is taken of an argument raised by S and
+// the factor 2^S is taken back out of the partner operand of the final
+// product, which costs nothing: for GELU out of the reciprocal (its
+// constants carry 2^S), for SiLU and sigmoid out of the denominator.  S is
+// the smallest shift that keeps every product representable in the output
+// type (fp16 outputs underflow long before 2^-126, so S = 0 there).
+//
+// |x| * tail uses the multiply in which 0 * x = 0 for every x, so x = +-inf
+// (where the tail is 0) gives relu(x) exactly without a separate clamp.  The
+// absolute value is a source modifier of the instruction.
+__device__ inline float abs_mul_zero_wins(float x, float b) {
+  float r;
+  asm("v_mul_legacy_f32_e64 %0, |%1|, %2" : "=v"(r) : "v"(x), "v"(b));
+  return r;
+}
+
+// max(x, -0) as one integer op: the unsigned minimum with the bits of -0
+// keeps every float with the sign bit clear (+inf, NaN included) and maps
+// every negative input to -0.
+__device__ inline float relu(float x) {
+  return __uint_as_float(min(__float_as_uint(x), 0x80000000u));
+}
+
+constexpr double pow2(int e) {
+  double r = 1.0;
+  for (int i = 0; i < (e < 0 ? -e : e); ++i) r = (e < 0) ? r * 0.5 : r * 2.0;
+  return r;
+}
+
+// GELU: the normal upper tail Q(t) = P(Z > t) = r exp2(c(r) - t^2/(2 ln 2))
+// with r = 1/(1 + p t) and c a polynomial in r (the form of the Chebyshev
+// fitted erfc of Numerical Recipes, coefficients fitted here for a minimal
+// maximum relative error on t in [0, 15]):
+//   degree 3: max rel. error 1.9e-4  (bf16 results: within 1 ulp)
+//   degree 4: max rel. error 5.5e-5  (fp16 results: within 1 ulp)
+//   degree 6: max rel. error 1.3e-6  (fp32 results: within 1e-5 rel / 2e-6 abs)
+template <int DEG>
+struct QFit;
+template <>
+struct QFit<3> {
+  static constexpr float p = 0.36950944455033363f;
+  static constexpr float c[4] = {-2.7541667327185095f, 1.3469623570975156f,
+                                 0.9101290363759839f, -0.5032013588354882f};
+};
+template <>
+struct QFit<4> {
+  static constexpr float p = 0.5063964087913556f;
+  static constexpr float c[5] = {-2.3043683184461905f, 1.3894173139728148f,
+                                 0.6817571899264395f, -1.149862878045882f,
+                                 0.38313433006936115f};
+};
+template <>
+struct QFit<6> {
+  static constexpr float p = 0.2715552190762726f;
+  static constexpr float c[7] = {-3.204975453658058f, 1.4179583422514952f,
+                                 0.7853715466157367f, -0.343943261631901f,
+                                 1.2761535905064931f, -1.3184075229241483f,
+                                 0.3878445554240053f};
+};
+
+// Per output type: GELU polynomial degree and the exponent shifts S.
+template <int DT>
+struct Prec {                       // fp32
+  static constexpr int kGeluDeg = 6, kGeluS = 20, kSiluS = 32, kSigmoidS = 24;
+};
+template <>
+struct Prec<FEWBIT_BF16> {
+  static constexpr int kGeluDeg = 3, kGeluS = 16, kSiluS = 16, kSigmoidS = 16;
+};
+template <>
+struct Prec<FEWBIT_F16> {
+  static constexpr int kGeluDeg = 4, kGeluS = 0, kSiluS = 0, kSigmoidS = 0;
+};
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kHalfLog2e = 0.7213475204444817f;   // 1/(2 ln 2)
+
+template <int DT, int ACT>
 struct Act;
 
-template <>
-struct Act<FEWBIT_GELU> {
+template <int DT>
+struct Act<DT, FEWBIT_GELU> {
+  static constexpr int D = Prec<DT>::kGeluDeg, S = Prec<DT>::kGeluS;
+  using F = QFit<D>;
+  // coefficients of c in r' = 2^-S r: c_i 2^(S i), and c_0 + S
+  static constexpr float coef(int i) {
+    return i == 0 ? F::c[0] + static_cast<float>(S)
+                  : static_cast<float>(static_cast<double>(F::c[i]) * pow2(S * i));
+  }
   __device__ static float f(float x) {
     const float t = fabsf(x);
-    const float q = 0.5f * erfcf(t * 0.70710678118654752f);   // P(Z > |x|)
-    float y = (x >= 0.0f) ? fmaf(-x, q, x) : x * q;
-    if (__builtin_isinf(x)) y = (x > 0.0f) ? x : -0.0f;
-    return y;
+    const float rs = __builtin_amdgcn_rcpf(
+        fmaf(t, static_cast<float>(F::p * pow2(S)), static_cast<float>(pow2(S))));  // 2^-S r
+    float c = coef(D);
+#pragma unroll
+    for (int i = D - 1; i >= 0; --i) c = fmaf(c, rs, coef(i));
+    const float e = __builtin_amdgcn_exp2f(fmaf(x * x, -kHalfLog2e, c));    // 2^S Q(t) / r
+    return fmaf(-abs_mul_zero_wins(x, rs), e, relu(x));   // relu(x) - t Q(t); NaN via x*x
   }
 };
 
-template <>
-struct Act<FEWBIT_SILU> {
+template <int DT>
+struct Act<DT, FEWBIT_SILU> {
+  static constexpr int S = Prec<DT>::kSiluS;
   __device__ static float f(float x) {
     const float t = fabsf(x);
-    const float e = expf(-t);
-    const float tail = e / (1.0f + e);                          // sigmoid(-|x|)
-    float y = (x >= 0.0f) ? fmaf(-x, tail, x) : x * tail;
-    if (__builtin_isinf(x)) y = (x > 0.0f) ? x : -0.0f;
-    return y;
+    const float e = __builtin_amdgcn_exp2f(fmaf(t, -kLog2e, static_cast<float>(S)));  // 2^S e^-t
+    const float r = __builtin_amdgcn_rcpf(e + static_cast<float>(pow2(S)));  // 1/(2^S (1 + e^-t))
+    return fmaf(-abs_mul_zero_wins(x, e), r, relu(x));    // relu(x) - t sigma(-t)
   }
 };
 
-template <>
-struct Act<FEWBIT_SIGMOID> {
+template <int DT>
+struct Act<DT, FEWBIT_SIGMOID> {
+  static constexpr int S = Prec<DT>::kSigmoidS;
   __device__ static float f(float x) {
-    const float e = expf(-fabsf(x));
-    const float r = 1.0f / (1.0f + e);                          // sigmoid(|x|)
-    return (x >= 0.0f) ? r : (x < 0.0f ? e * r : x);            // NaN -> NaN
+    const float t = fabsf(x);
+    const float e = __builtin_amdgcn_exp2f(fmaf(t, -kLog2e, static_cast<float>(S)));  // 2^S e^-t
+    const float r = __builtin_amdgcn_rcpf(e + static_cast<float>(pow2(S)));  // 1/(2^S (1 + e^-t))
+    return ((x >= 0.0f) ? static_cast<float>(pow2(S)) : e) * r;   // NaN: e * r is NaN
   }
 };
 
-template <>
-struct Act<FEWBIT_TANH> {
+template <int DT>
+struct Act<DT, FEWBIT_TANH> {
   __device__ static float f(float x) { return tanhf(x); }
 };
 
@@ -184,6 +300,30 @@ __device__ inline uint32_t classify(float x, const TableArgs& tab) {
   return c;
 }
 
+// Interval index of every 16-bit input pattern, one byte each.
+template <int DT, int BITS>
+__device__ void build_code_table(uint8_t* lut, const TableArgs& tab, int symmetric) {
+  auto code_of = [&](uint32_t p) {
+    const float v = Half<DT>::widen(p);
+    return classify<BITS>(symmetric ? fabsf(v) : v, tab);
+  };
+  for (uint32_t run = threadIdx.x; run < 4096u; run += blockDim.x) {
+    const uint32_t p0 = run * 16u;
+    const uint32_t a = code_of(p0), b = code_of(p0 + 15u);
+    u32x4_t w;
+    if (!Half<DT>::special_run(p0) && a == b) {
+      const uint32_t rep = a * 0x01010101u;
+      w = (u32x4_t){rep, rep, rep, rep};
+    } else {
+      uint32_t q[4] = {0u, 0u, 0u, 0u};
+      for (uint32_t k = 0; k < 16u; ++k) q[k >> 2] |= code_of(p0 + k) << (8u * (k & 3u));
+      w = (u32x4_t){q[0], q[1], q[2], q[3]};
+    }
+    *reinterpret_cast<u32x4_t*>(lut + p0) = w;
+  }
+  __syncthreads();
+}
+
 // ---------------------------------------------------------------- packing
 // quad_perm DPP control: lane k of each quad reads lane sel[k] of the quad.
 constexpr int quad_perm(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
@@ -191,6 +331,15 @@ constexpr int quad_perm(int a, int b, int c, int d) { return a | (b << 2) | (c <
 template <int CTRL>
 __device__ inline uint32_t quad_read(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), CTRL, 0xF, 0xF, false));
+}
+
+__device__ inline void st_word(uint32_t* p, uint32_t v) {
+  if constexpr (FEWBIT_NT_STORES) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+__device__ inline uint32_t ld_word(const uint32_t* p) {
+  if constexpr (FEWBIT_NT_LOADS) return __builtin_nontemporal_load(p);
+  return *p;
 }
 
 // Lane field F holds the 8 codes of the lane (8*BITS bits, code j at bit
@@ -201,123 +350,302 @@ __device__ inline uint32_t quad_read(uint32_t v) {
 template <int BITS>
 __device__ inline void pack_store(uint32_t* out, uint32_t F, int lane, int64_t valid) {
   if constexpr (BITS == 4) {
-    if (lane < valid) out[lane] = F;
+    if (lane < valid) st_word(out + lane, F);
   } else if constexpr (BITS == 2) {
     const uint32_t nb = quad_read<quad_perm(1, 1, 3, 3)>(F);
     const uint32_t w = F | (nb << 16);
     const int widx = lane >> 1;
-    if (!(lane & 1) && widx < valid) out[widx] = w;
+    if (!(lane & 1) && widx < valid) st_word(out + widx, w);
   } else if constexpr (BITS == 1) {
     const uint32_t n1 = quad_read<quad_perm(1, 1, 3, 3)>(F);
     const uint32_t a = F | (n1 << 8);
     const uint32_t n2 = quad_read<quad_perm(2, 2, 2, 2)>(a);
     const uint32_t w = a | (n2 << 16);
     const int widx = lane >> 2;
-    if (!(lane & 3) && widx < valid) out[widx] = w;
+    if (!(lane & 3) && widx < valid) st_word(out + widx, w);
   } else {  // BITS == 3: a quad's 4 x 24 bits are words 3q, 3q+1, 3q+2
     const uint32_t nx = quad_read<quad_perm(1, 2, 3, 3)>(F);
     const int k = lane & 3;
     const uint32_t w = (F >> (8 * k)) | (nx << (24 - 8 * k));
     const int widx = 3 * (lane >> 2) + k;
-    if (k < 3 && widx < valid) out[widx] = w;
+    if (k < 3 && widx < valid) st_word(out + widx, w);
   }
 }
 
-// Inverse of the layout above: the lane's 8*BITS-bit field.
+// Inverse of the layout above: the lane's 8*BITS-bit field.  For 1, 2 and 4
+// bits a field lies inside one word (lanes that share a word read the same
+// address).  For 3 bits lanes 0..2 of each quad read the quad's 3 words with
+// one coalesced load; each lane then takes its own word and the one before
+// it from the quad and funnel-shifts its 24 bits out.  Must be called by all
+// 64 lanes together.
 template <int BITS>
 __device__ inline uint32_t load_field(const uint32_t* base, int lane, int64_t valid) {
-  const int bit = 8 * BITS * lane;
-  const int w = bit >> 5, sh = bit & 31;
-  const uint32_t lo = (w < valid) ? base[w] : 0u;
-  if (sh + 8 * BITS > 32) {
-    const uint32_t hi = (w + 1 < valid) ? base[w + 1] : 0u;
-    return __builtin_amdgcn_alignbit(hi, lo, sh);
+  if constexpr (BITS == 3) {
+    const int k = lane & 3;
+    const int widx = 3 * (lane >> 2) + k;
+    const uint32_t w = (k < 3 && widx < valid) ? ld_word(base + widx) : 0u;
+    const uint32_t prev = quad_read<quad_perm(0, 0, 1, 2)>(w);   // word k-1 (k = 0: word 0)
+    const uint32_t own = quad_read<quad_perm(0, 1, 2, 2)>(w);    // word k (k = 3: word 2)
+    return __builtin_amdgcn_alignbit(own, prev, (24 * k) & 31);
+  } else {
+    const int widx = (8 * BITS * lane) >> 5;
+    const uint32_t v = (widx < valid) ? ld_word(base + widx) : 0u;
+    return v >> ((8 * BITS * lane) & 31);
   }
-  return lo >> sh;
 }
 
-// ---------------------------------------------------------------- kernels
+struct WaveIndex {
+  int lane;
+  int64_t wave, nwaves;
+};
+__device__ inline WaveIndex wave_index() {
+  const int per_block = blockDim.x / kWave;
+  return {static_cast<int>(threadIdx.x & (kWave - 1)),
+          static_cast<int64_t>(blockIdx.x) * per_block + (threadIdx.x / kWave),
+          static_cast<int64_t>(gridDim.x) * per_block};
+}
+
+// ---------------------------------------------------------------- forward, fp16 / bf16
 template <int DT, int BITS, int ACT>
-__global__ __launch_bounds__(kBlock) void fwd_kernel(const void* x, void* y,
-                                                     uint32_t* __restrict__ codes,
-                                                     int64_t n, int64_t nwords,
-                                                     TableArgs tab, int symmetric) {
-  using S = Storage<DT>;
-  constexpr int kWordsPerTile = 16 * BITS;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int64_t wave = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
-  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
-  const int64_t full = n / kTile;
-
-  for (int64_t t = wave; t < full; t += nwaves) {
-    const int64_t e = t * kTile + static_cast<int64_t>(lane) * kPerLane;
-    float xf[8], yf[8];
-    S::load8(x, e, xf);
-    uint32_t F = 0;
+__device__ inline void fwd16_tile(u32x4_t in, const uint8_t* lut, u32x4_t& out, uint32_t& F) {
+  using H = Half<DT>;
+  F = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      yf[j] = Act<ACT>::f(xf[j]);
-      const float xc = symmetric ? fabsf(xf[j]) : xf[j];
-      F |= classify<BITS>(xc, tab) << (BITS * j);
-    }
-    S::store8(y, e, yf);
-    pack_store<BITS>(codes + t * kWordsPerTile, F, lane, kWordsPerTile);
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t w = in[k];
+    const uint32_t c0 = lut[w & 0xFFFFu], c1 = lut[w >> 16];
+    const float y0 = Act<DT, ACT>::f(H::lo(w)), y1 = Act<DT, ACT>::f(H::hi(w));
+    out[k] = H::pack(y0, y1);
+    F |= (c0 << (2 * k * BITS)) | (c1 << ((2 * k + 1) * BITS));
   }
+}
 
+template <int DT, int BITS, int ACT>
+__global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
+    const uint16_t* x, uint16_t* y, uint32_t* __restrict__ codes, int64_t n, int64_t nwords,
+    TableArgs tab, int symmetric) {
+  constexpr int U = FEWBIT_FWD16_UNROLL;
+  constexpr int kWords = 16 * BITS;
+  __shared__ __attribute__((aligned(16))) uint8_t lut[65536];
+  build_code_table<DT, BITS>(lut, tab, symmetric);
+
+  const WaveIndex wi = wave_index();
+  const int64_t full = n / kTile;
+  const int64_t groups = full / U;
+  const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
+
+  for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
+    const int64_t t0 = gi * U;
+    u32x4_t in[U], out[U];
+    uint32_t F[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (t0 + u) * kTile + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u) fwd16_tile<DT, BITS, ACT>(in[u], lut, out[u], F[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
+      pack_store<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane, kWords);
+    }
+  }
+  for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
+    u32x4_t out;
+    uint32_t F;
+    fwd16_tile<DT, BITS, ACT>(ld_stream(x + t * kTile + lane_off), lut, out, F);
+    st_stream(y + t * kTile + lane_off, out);
+    pack_store<BITS>(codes + t * kWords, F, wi.lane, kWords);
+  }
   // the partial tile at the end, if any, goes to the wave that would own it
-  if (n % kTile != 0 && wave == full % nwaves) {
+  if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
     const int64_t t = full;
     uint32_t F = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int64_t e = t * kTile + static_cast<int64_t>(lane) * kPerLane + j;
+    for (int j = 0; j < kPerLane; ++j) {
+      const int64_t e = t * kTile + lane_off + j;
       if (e < n) {
-        const float xv = S::load1(x, e);
-        S::store1(y, e, Act<ACT>::f(xv));
-        const float xc = symmetric ? fabsf(xv) : xv;
-        F |= classify<BITS>(xc, tab) << (BITS * j);
+        const uint32_t bits16 = x[e];
+        Scalar<DT>::store(y, e, Act<DT, ACT>::f(Half<DT>::widen(bits16)));
+        F |= static_cast<uint32_t>(lut[bits16]) << (BITS * j);
       }
     }
-    const int64_t wbase = t * kWordsPerTile;
-    pack_store<BITS>(codes + wbase, F, lane, nwords - wbase);
+    const int64_t wbase = t * kWords;
+    pack_store<BITS>(codes + wbase, F, wi.lane, nwords - wbase);
   }
+}
+
+// ---------------------------------------------------------------- forward, fp32
+template <int BITS, int ACT>
+__device__ inline void fwd32_tile(const u32x4_t (&in)[2], const TableArgs& tab, int symmetric,
+                                  u32x4_t (&out)[2], uint32_t& F) {
+  F = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float xv = __uint_as_float(in[j >> 2][j & 3]);
+    out[j >> 2][j & 3] = __float_as_uint(Act<FEWBIT_F32, ACT>::f(xv));
+    F |= classify<BITS>(symmetric ? fabsf(xv) : xv, tab) << (BITS * j);
+  }
+}
+
+template <int BITS, int ACT>
+__global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
+    const float* x, float* y, uint32_t* __restrict__ codes, int64_t n, int64_t nwords,
+    TableArgs tab, int symmetric) {
+  constexpr int U = FEWBIT_FWD32_UNROLL;
+  constexpr int kWords = 16 * BITS;
+  const WaveIndex wi = wave_index();
+  const int64_t full = n / kTile;
+  const int64_t groups = full / U;
+  const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
+
+  for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
+    const int64_t t0 = gi * U;
+    u32x4_t in[U][2], out[U][2];
+    uint32_t F[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float* p = x + (t0 + u) * kTile + lane_off;
+      in[u][0] = ld_stream(p);
+      in[u][1] = ld_stream(p + 4);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) fwd32_tile<BITS, ACT>(in[u], tab, symmetric, out[u], F[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float* q = y + (t0 + u) * kTile + lane_off;
+      st_stream(q, out[u][0]);
+      st_stream(q + 4, out[u][1]);
+      pack_store<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane, kWords);
+    }
+  }
+  for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
+    const float* p = x + t * kTile + lane_off;
+    const u32x4_t in[2] = {ld_stream(p), ld_stream(p + 4)};
+    u32x4_t out[2];
+    uint32_t F;
+    fwd32_tile<BITS, ACT>(in, tab, symmetric, out, F);
+    st_stream(y + t * kTile + lane_off, out[0]);
+    st_stream(y + t * kTile + lane_off + 4, out[1]);
+    pack_store<BITS>(codes + t * kWords, F, wi.lane, kWords);
+  }
+  if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
+    const int64_t t = full;
+    uint32_t F = 0;
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) {
+      const int64_t e = t * kTile + lane_off + j;
+      if (e < n) {
+        const float xv = x[e];
+        y[e] = Act<FEWBIT_F32, ACT>::f(xv);
+        F |= classify<BITS>(symmetric ? fabsf(xv) : xv, tab) << (BITS * j);
+      }
+    }
+    const int64_t wbase = t * kWords;
+    pack_store<BITS>(codes + wbase, F, wi.lane, nwords - wbase);
+  }
+}
+
+// ---------------------------------------------------------------- backward
+// The values of two consecutive elements come from one 8-byte LDS read: the
+// pair table holds (v[c0], v[c1]) at index c0 | c1 << BITS, which is exactly
+// the 2*BITS-bit slice of the lane field holding the two codes.
+template <int BITS>
+__device__ inline f32x2_t pair_values(const f32x2_t* pairs, uint32_t F, int pair) {
+  return pairs[(F >> (2 * BITS * pair)) & ((1u << (2 * BITS)) - 1u)];
 }
 
 template <int DT, int BITS>
-__global__ __launch_bounds__(kBlock) void bwd_kernel(const void* g,
-                                                     const uint32_t* __restrict__ codes,
-                                                     void* gin, int64_t n, int64_t nwords,
-                                                     TableArgs tab) {
-  using S = Storage<DT>;
-  constexpr int kWordsPerTile = 16 * BITS;
-  constexpr uint32_t kMask = (1u << BITS) - 1u;
-  __shared__ float val[16];
-  if (threadIdx.x < 16) val[threadIdx.x] = tab.v[threadIdx.x];
-  __syncthreads();
-
-  const int lane = threadIdx.x & (kWave - 1);
-  const int64_t wave = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
-  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
-  const int64_t full = n / kTile;
-
-  for (int64_t t = wave; t < full; t += nwaves) {
-    const int64_t e = t * kTile + static_cast<int64_t>(lane) * kPerLane;
-    float gf[8];
-    S::load8(g, e, gf);
-    const uint32_t F = load_field<BITS>(codes + t * kWordsPerTile, lane, kWordsPerTile);
+struct Grad {
+  static constexpr int kVecs = 1;   // 16-byte vectors per lane per tile
+  __device__ static void apply(const u32x4_t (&g)[1], uint32_t F, const f32x2_t* pairs,
+                               u32x4_t (&out)[1]) {
+    using H = Half<DT>;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) gf[j] = gf[j] * val[(F >> (BITS * j)) & kMask];
-    S::store8(gin, e, gf);
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t w = g[0][k];
+      const f32x2_t v = pair_values<BITS>(pairs, F, k);
+      out[0][k] = H::pack(H::lo(w) * v.x, H::hi(w) * v.y);   // fp32 products, then RNE
+    }
   }
+};
 
-  if (n % kTile != 0 && wave == full % nwaves) {
-    const int64_t t = full;
-    const int64_t wbase = t * kWordsPerTile;
-    const uint32_t F = load_field<BITS>(codes + wbase, lane, nwords - wbase);
+template <int BITS>
+struct Grad<FEWBIT_F32, BITS> {
+  static constexpr int kVecs = 2;
+  __device__ static void apply(const u32x4_t (&g)[2], uint32_t F, const f32x2_t* pairs,
+                               u32x4_t (&out)[2]) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int64_t e = t * kTile + static_cast<int64_t>(lane) * kPerLane + j;
-      if (e < n) S::store1(gin, e, S::load1(g, e) * val[(F >> (BITS * j)) & kMask]);
+    for (int k = 0; k < 4; ++k) {
+      const f32x2_t v = pair_values<BITS>(pairs, F, k);
+      const int a = 2 * k, b = 2 * k + 1;
+      out[a >> 2][a & 3] = __float_as_uint(__uint_as_float(g[a >> 2][a & 3]) * v.x);
+      out[b >> 2][b & 3] = __float_as_uint(__uint_as_float(g[b >> 2][b & 3]) * v.y);
+    }
+  }
+};
+
+template <int DT, int BITS>
+__global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
+    const void* g, const uint32_t* __restrict__ codes, void* gin, int64_t n, int64_t nwords,
+    TableArgs tab) {
+  constexpr int U = FEWBIT_BWD_UNROLL;
+  constexpr int V = Grad<DT, BITS>::kVecs;
+  constexpr int kWords = 16 * BITS;
+  constexpr int kEsz = (DT == FEWBIT_F32) ? 4 : 2;
+  constexpr uint32_t kMask = (1u << BITS) - 1u;
+  constexpr int kPairs = 1 << (2 * BITS);
+  __shared__ f32x2_t pairs[kPairs];
+  for (int i = threadIdx.x; i < kPairs; i += blockDim.x)
+    pairs[i] = (f32x2_t){tab.v[i & kMask], tab.v[i >> BITS]};
+  __syncthreads();
+  const float* val = reinterpret_cast<const float*>(pairs);   // val[2c] = v[c] (c < K)
+
+  const WaveIndex wi = wave_index();
+  const int64_t full = n / kTile;
+  const int64_t groups = full / U;
+  const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
+  const char* gb = static_cast<const char*>(g);
+  char* ob = static_cast<char*>(gin);
+
+  for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
+    const int64_t t0 = gi * U;
+    u32x4_t in[U][V], out[U][V];
+    uint32_t F[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const char* p = gb + ((t0 + u) * kTile + lane_off) * kEsz;
+#pragma unroll
+      for (int v = 0; v < V; ++v) in[u][v] = ld_stream(p + 16 * v);
+      F[u] = load_field<BITS>(codes + (t0 + u) * kWords, wi.lane, kWords);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) Grad<DT, BITS>::apply(in[u], F[u], pairs, out[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      char* q = ob + ((t0 + u) * kTile + lane_off) * kEsz;
+#pragma unroll
+      for (int v = 0; v < V; ++v) st_stream(q + 16 * v, out[u][v]);
+    }
+  }
+  for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
+    u32x4_t in[V], out[V];
+    const char* p = gb + (t * kTile + lane_off) * kEsz;
+#pragma unroll
+    for (int v = 0; v < V; ++v) in[v] = ld_stream(p + 16 * v);
+    const uint32_t F = load_field<BITS>(codes + t * kWords, wi.lane, kWords);
+    Grad<DT, BITS>::apply(in, F, pairs, out);
+    char* q = ob + (t * kTile + lane_off) * kEsz;
+#pragma unroll
+    for (int v = 0; v < V; ++v) st_stream(q + 16 * v, out[v]);
+  }
+  if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
+    const int64_t t = full;
+    const int64_t wbase = t * kWords;
+    const uint32_t F = load_field<BITS>(codes + wbase, wi.lane, nwords - wbase);
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) {
+      const int64_t e = t * kTile + lane_off + j;
+      if (e < n)
+        Scalar<DT>::store(gin, e, Scalar<DT>::load(g, e) * val[2 * ((F >> (BITS * j)) & kMask)]);
     }
   }
 }
@@ -338,17 +666,6 @@ int check_table(const fewbit_table* t) {
   return FEWBIT_OK;
 }
 
-// Status of the launch just made; with FEWBIT_DEBUG set in the environment
-// the HIP error behind FEWBIT_E_HIP is printed to stderr.
-int launch_status(const char* where) {
-  const hipError_t e = hipGetLastError();
-  if (e == hipSuccess) return FEWBIT_OK;
-  if (std::getenv("FEWBIT_DEBUG"))
-    std::fprintf(stderr, "fewbit: %s launch failed: %s (%s)\n", where, hipGetErrorName(e),
-                 hipGetErrorString(e));
-  return FEWBIT_E_HIP;
-}
-
 bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
 TableArgs table_args(const fewbit_table* t) {
@@ -359,61 +676,112 @@ TableArgs table_args(const fewbit_table* t) {
   return a;
 }
 
-dim3 grid_for(int64_t n) {
+// Compute units of the current device, cached per device (the only state the
+// library keeps).
+int device_cus() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+  if (dev >= 0 && dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int c = 0;
+  if (dev < 0 ||
+      hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      c <= 0)
+    c = 256;
+  if (dev >= 0 && dev < 64) cache[dev].store(c, std::memory_order_relaxed);
+  return c;
+}
+
+dim3 grid_for(int64_t n, int threads, int wg_per_cu) {
   const int64_t tiles = (n + kTile - 1) / kTile;
-  int64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
-  if (blocks > kMaxBlocks) blocks = kMaxBlocks;
+  const int waves_per_block = threads / kWave;
+  int64_t blocks = (tiles + waves_per_block - 1) / waves_per_block;
+  const int64_t cap = static_cast<int64_t>(device_cus()) * wg_per_cu;
+  if (blocks > cap) blocks = cap;
   if (blocks < 1) blocks = 1;
   return dim3(static_cast<unsigned>(blocks));
 }
 
+struct Launch {
+  const fewbit_table* t;
+  const void* in;
+  void* out;
+  uint32_t* codes;
+  int64_t n;
+  hipStream_t s;
+};
+
 template <int DT, int BITS, int ACT>
-void launch_fwd(const fewbit_table* t, const void* x, void* y, uint32_t* codes, int64_t n,
-                hipStream_t s) {
-  const int64_t nw = (n * BITS + 31) / 32;
-  hipLaunchKernelGGL((fwd_kernel<DT, BITS, ACT>), grid_for(n), dim3(kBlock), 0, s, x, y, codes,
-                     n, nw, table_args(t), (t->flags & FEWBIT_FLAG_SYMMETRIC) ? 1 : 0);
-}
-
-template <int DT, int BITS>
-void launch_fwd_act(const fewbit_table* t, const void* x, void* y, uint32_t* codes, int64_t n,
-                    hipStream_t s) {
-  switch (t->act) {
-    case FEWBIT_GELU: launch_fwd<DT, BITS, FEWBIT_GELU>(t, x, y, codes, n, s); break;
-    case FEWBIT_SILU: launch_fwd<DT, BITS, FEWBIT_SILU>(t, x, y, codes, n, s); break;
-    case FEWBIT_SIGMOID: launch_fwd<DT, BITS, FEWBIT_SIGMOID>(t, x, y, codes, n, s); break;
-    default: launch_fwd<DT, BITS, FEWBIT_TANH>(t, x, y, codes, n, s); break;
-  }
-}
-
-template <int DT>
-void launch_fwd_bits(const fewbit_table* t, const void* x, void* y, uint32_t* codes, int64_t n,
-                     hipStream_t s) {
-  switch (t->bits) {
-    case 1: launch_fwd_act<DT, 1>(t, x, y, codes, n, s); break;
-    case 2: launch_fwd_act<DT, 2>(t, x, y, codes, n, s); break;
-    case 3: launch_fwd_act<DT, 3>(t, x, y, codes, n, s); break;
-    default: launch_fwd_act<DT, 4>(t, x, y, codes, n, s); break;
+void launch_fwd(const Launch& L) {
+  const int64_t nw = (L.n * BITS + 31) / 32;
+  const int sym = (L.t->flags & FEWBIT_FLAG_SYMMETRIC) ? 1 : 0;
+  if constexpr (DT == FEWBIT_F32) {
+    const dim3 grid = grid_for(L.n, FEWBIT_FWD32_THREADS, FEWBIT_FWD32_WG_PER_CU);
+    (void)hipGetLastError();
+    hipLaunchKernelGGL((fwd32_kernel<BITS, ACT>), grid, dim3(FEWBIT_FWD32_THREADS), 0, L.s,
+                       static_cast<const float*>(L.in), static_cast<float*>(L.out), L.codes, L.n,
+                       nw, table_args(L.t), sym);
+  } else {
+    const dim3 grid = grid_for(L.n, FEWBIT_FWD16_THREADS, FEWBIT_FWD16_WG_PER_CU);
+    (void)hipGetLastError();
+    hipLaunchKernelGGL((fwd16_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16_THREADS), 0, L.s,
+                       static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
+                       L.n, nw, table_args(L.t), sym);
   }
 }
 
 template <int DT, int BITS>
-void launch_bwd(const fewbit_table* t, const void* g, const uint32_t* codes, void* gin, int64_t n,
-                hipStream_t s) {
-  const int64_t nw = (n * BITS + 31) / 32;
-  hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid_for(n), dim3(kBlock), 0, s, g, codes, gin, n,
-                     nw, table_args(t));
+void launch_fwd_act(const Launch& L) {
+  switch (L.t->act) {
+    case FEWBIT_GELU: launch_fwd<DT, BITS, FEWBIT_GELU>(L); break;
+    case FEWBIT_SILU: launch_fwd<DT, BITS, FEWBIT_SILU>(L); break;
+    case FEWBIT_SIGMOID: launch_fwd<DT, BITS, FEWBIT_SIGMOID>(L); break;
+    default: launch_fwd<DT, BITS, FEWBIT_TANH>(L); break;
+  }
 }
 
 template <int DT>
-void launch_bwd_bits(const fewbit_table* t, const void* g, const uint32_t* codes, void* gin,
-                     int64_t n, hipStream_t s) {
-  switch (t->bits) {
-    case 1: launch_bwd<DT, 1>(t, g, codes, gin, n, s); break;
-    case 2: launch_bwd<DT, 2>(t, g, codes, gin, n, s); break;
-    case 3: launch_bwd<DT, 3>(t, g, codes, gin, n, s); break;
-    default: launch_bwd<DT, 4>(t, g, codes, gin, n, s); break;
+void launch_fwd_bits(const Launch& L) {
+  switch (L.t->bits) {
+    case 1: launch_fwd_act<DT, 1>(L); break;
+    case 2: launch_fwd_act<DT, 2>(L); break;
+    case 3: launch_fwd_act<DT, 3>(L); break;
+    default: launch_fwd_act<DT, 4>(L); break;
   }
+}
+
+template <int DT, int BITS>
+void launch_bwd(const Launch& L) {
+  const int64_t nw = (L.n * BITS + 31) / 32;
+  const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS, FEWBIT_BWD_WG_PER_CU);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s, L.in,
+                     L.codes, L.out, L.n, nw, table_args(L.t));
+}
+
+template <int DT>
+void launch_bwd_bits(const Launch& L) {
+  switch (L.t->bits) {
+    case 1: launch_bwd<DT, 1>(L); break;
+    case 2: launch_bwd<DT, 2>(L); break;
+    case 3: launch_bwd<DT, 3>(L); break;
+    default: launch_bwd<DT, 4>(L); break;
+  }
+}
+
+// Status of the launch just made (the runtime's last-error slot was cleared
+// right before it); with FEWBIT_DEBUG set in the environment the HIP error
+// behind FEWBIT_E_HIP is printed to stderr.
+int launch_status(const char* where) {
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) return FEWBIT_OK;
+  if (std::getenv("FEWBIT_DEBUG"))
+    std::fprintf(stderr, "fewbit: %s launch failed: %s (%s)\n", where, hipGetErrorName(e),
+                 hipGetErrorString(e));
+  return FEWBIT_E_HIP;
 }
 
 }  // namespace
@@ -427,15 +795,11 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   if (n == 0) return FEWBIT_OK;
   if (!x || !y || !codes) return FEWBIT_E_NULL;
   if (misaligned(x) || misaligned(y) || misaligned(codes)) return FEWBIT_E_ALIGN;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  // the runtime's last-error slot may hold an error left by an earlier,
-  // unrelated call on this thread; clear it so the check below sees only
-  // this launch
-  (void)hipGetLastError();
+  const Launch L{t, x, y, codes, n, static_cast<hipStream_t>(stream)};
   switch (dtype) {
-    case FEWBIT_F32: launch_fwd_bits<FEWBIT_F32>(t, x, y, codes, n, s); break;
-    case FEWBIT_F16: launch_fwd_bits<FEWBIT_F16>(t, x, y, codes, n, s); break;
-    default: launch_fwd_bits<FEWBIT_BF16>(t, x, y, codes, n, s); break;
+    case FEWBIT_F32: launch_fwd_bits<FEWBIT_F32>(L); break;
+    case FEWBIT_F16: launch_fwd_bits<FEWBIT_F16>(L); break;
+    default: launch_fwd_bits<FEWBIT_BF16>(L); break;
   }
   return launch_status("fewbit_fwd");
 }
@@ -449,12 +813,12 @@ extern "C" int fewbit_bwd(const fewbit_table* t, int32_t dtype, const void* grad
   if (n == 0) return FEWBIT_OK;
   if (!grad_out || !codes || !grad_in) return FEWBIT_E_NULL;
   if (misaligned(grad_out) || misaligned(codes) || misaligned(grad_in)) return FEWBIT_E_ALIGN;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  (void)hipGetLastError();  // see fewbit_fwd
+  const Launch L{t, grad_out, grad_in, const_cast<uint32_t*>(codes), n,
+                 static_cast<hipStream_t>(stream)};
   switch (dtype) {
-    case FEWBIT_F32: launch_bwd_bits<FEWBIT_F32>(t, grad_out, codes, grad_in, n, s); break;
-    case FEWBIT_F16: launch_bwd_bits<FEWBIT_F16>(t, grad_out, codes, grad_in, n, s); break;
-    default: launch_bwd_bits<FEWBIT_BF16>(t, grad_out, codes, grad_in, n, s); break;
+    case FEWBIT_F32: launch_bwd_bits<FEWBIT_F32>(L); break;
+    case FEWBIT_F16: launch_bwd_bits<FEWBIT_F16>(L); break;
+    default: launch_bwd_bits<FEWBIT_BF16>(L); break;
   }
   return launch_status("fewbit_bwd");
 }
