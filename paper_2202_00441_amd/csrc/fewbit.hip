@@ -45,7 +45,7 @@
 // the tiles) and tiles in flight per wave, per kernel.  The fp16 / bf16
 // forward holds a 64 KiB table per workgroup, so at most 2 fit per CU.
 #ifndef FEWBIT_FWD16_THREADS
-#define FEWBIT_FWD16_THREADS 256
+#define FEWBIT_FWD16_THREADS 512
 #endif
 #ifndef FEWBIT_FWD16_WG_PER_CU
 #define FEWBIT_FWD16_WG_PER_CU 2
