@@ -12,6 +12,7 @@ algorithmic bytes: forward reads x (s bytes) and writes y (s) and codes
 (b/8); backward reads grad_out (s) and codes (b/8) and writes grad_in (s).
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--bits B]
+  python bench.py --summarize-trace DIR [--summarize-counters FETCH_DIR WRITE_DIR]
 """
 import argparse
 import hashlib
@@ -55,6 +56,106 @@ def measured_traffic(workload: str, bits: int, kernel: str):
     return rec.get("hbm_bytes") if rec else None
 
 
+# ---------------------------------------------------------------- rocprofv3 summaries
+DT_NAMES = {0: "f32", 1: "f16", 2: "bf16"}
+ACT_NAMES = {0: "gelu", 1: "silu", 2: "sigmoid", 3: "tanh"}
+
+
+def _kernel_key(name: str):
+    """'fwd16_kernel<bf16,3,gelu>' style key of a library kernel named in a
+    rocprofv3 csv, or the plain name for any other kernel."""
+    import re
+    m = re.search(r"(fwd16_kernel|fwd32_kernel|bwd_kernel)<([0-9, ]+)>", name)
+    if not m:
+        return name.split("(")[0]
+    args = [int(a) for a in m.group(2).split(",")]
+    if m.group(1) == "fwd16_kernel":
+        return f"fwd16_kernel<{DT_NAMES[args[0]]},{args[1]},{ACT_NAMES[args[2]]}>"
+    if m.group(1) == "fwd32_kernel":
+        return f"fwd32_kernel<f32,{args[0]},{ACT_NAMES[args[1]]}>"
+    return f"bwd_kernel<{DT_NAMES[args[0]]},{args[1]}>"
+
+
+def _csv(path):
+    import csv
+    with open(path, newline="") as fh:
+        return list(csv.DictReader(fh))
+
+
+def _one(directory, suffix):
+    import glob
+    hits = sorted(glob.glob(os.path.join(directory, "**", "*" + suffix), recursive=True))
+    if not hits:
+        raise SystemExit(f"no *{suffix} under {directory}")
+    return hits[0]
+
+
+def summarize_rocprof(trace_dir, fetch_dir, write_dir, workload, bits, out_traffic):
+    """Print the per-kernel summary of a `rocprofv3 --kernel-trace --stats`
+    run and, given the two counter runs (FETCH_SIZE, WRITE_SIZE), the HBM
+    bytes per launch of the library kernels, calibrated against the device
+    copy kernel of the same runs (which reads and writes `copy_bytes` each);
+    optionally store those bytes in profiles/traffic.json."""
+    import workloads as WL
+    w = WL.WORKLOADS[workload]
+    s = 4 if w.dtype == "f32" else 2
+    alg = algorithmic_bytes(w.n, w.dtype, bits)
+    copy_bytes = w.n * s
+    lines = []
+    if trace_dir:
+        lines.append("kernel                              calls   avg_us     min_us     max_us   "
+                     "alg_GB/s  frac_8TB/s")
+        for r in _csv(_one(trace_dir, "kernel_stats.csv")):
+            key = _kernel_key(r["Name"])
+            avg = float(r["AverageNs"]) / 1e3
+            is_lib = key.startswith(("fwd", "bwd"))
+            b = alg if is_lib else 2 * copy_bytes
+            gbps = b / (avg * 1e-6) / 1e9
+            lines.append(f"{key:34s} {int(r['Calls']):6d} {avg:9.2f} {float(r['MinNs']) / 1e3:10.2f} "
+                         f"{float(r['MaxNs']) / 1e3:10.2f} {gbps:10.1f} {gbps / HBM_PEAK_GBPS:10.4f}")
+    traffic = {}
+    if fetch_dir and write_dir:
+        per = {}
+        for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+            for r in _csv(_one(d, "counter_collection.csv")):
+                if r["Counter_Name"] != counter:
+                    continue
+                key = _kernel_key(r["Kernel_Name"])
+                per.setdefault(key, {}).setdefault(counter, []).append(
+                    float(r["Counter_Value"]) * 1024.0)
+        copy = [k for k in per if "copyBuffer" in k]
+        if not copy:
+            raise SystemExit("no device copy kernel in the counter runs to calibrate against")
+        cp = per[copy[0]]
+        f_fetch = copy_bytes / (sum(cp["FETCH_SIZE"]) / len(cp["FETCH_SIZE"]))
+        f_write = copy_bytes / (sum(cp["WRITE_SIZE"]) / len(cp["WRITE_SIZE"]))
+        lines.append("")
+        lines.append(f"calibration on {copy[0]} ({copy_bytes} B read + {copy_bytes} B written "
+                     f"per launch): FETCH_SIZE x {f_fetch:.4f}, WRITE_SIZE x {f_write:.4f}")
+        lines.append("kernel                              launches  fetch_B        write_B        "
+                     "hbm_B          alg_B          hbm/alg")
+        for key, c in sorted(per.items()):
+            if not key.startswith(("fwd", "bwd")) or "FETCH_SIZE" not in c or "WRITE_SIZE" not in c:
+                continue
+            fb = f_fetch * sum(c["FETCH_SIZE"]) / len(c["FETCH_SIZE"])
+            wb = f_write * sum(c["WRITE_SIZE"]) / len(c["WRITE_SIZE"])
+            lines.append(f"{key:34s} {len(c['FETCH_SIZE']):8d}  {fb:14.0f} {wb:14.0f} "
+                         f"{fb + wb:14.0f} {alg:14.0f} {(fb + wb) / alg:8.4f}")
+            kind = "fwd" if key.startswith("fwd") else "bwd"
+            traffic[f"{workload}/b{bits}/{kind}"] = {
+                "kernel": key, "fetch_bytes": round(fb), "write_bytes": round(wb),
+                "hbm_bytes": round(fb + wb), "algorithmic_bytes": alg}
+        if out_traffic:
+            rec = {"kernel_source_hash": kernel_source_hash(),
+                   "calibration": {"kernel": copy[0], "bytes_each_way": copy_bytes,
+                                   "fetch_factor": f_fetch, "write_factor": f_write},
+                   "launches": traffic}
+            with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as fh:
+                json.dump(rec, fh, indent=1)
+                fh.write("\n")
+    print("\n".join(lines))
+
+
 def cpu_baseline(w, bits, x_np, g_np, seconds=10.0, chunk=1 << 22):
     """The oracle, single-threaded, over consecutive chunks of the same input
     until `seconds` of CPU time have been spent.  It uses the oracle's own
@@ -95,11 +196,23 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="cfg4_gelu_bf16_lm_ffn")
+    ap.add_argument("--workload", default="gelu_bf16_lm_ffn_16x2048x8192")
     ap.add_argument("--bits", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="summarise a rocprofv3 --kernel-trace --stats output directory")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="calibrated HBM bytes from FETCH_SIZE and WRITE_SIZE runs")
+    ap.add_argument("--write-traffic", action="store_true",
+                    help="with --summarize-counters: store profiles/traffic.json")
     args = ap.parse_args()
+
+    if args.summarize_trace or args.summarize_counters:
+        fd, wd = args.summarize_counters or (None, None)
+        summarize_rocprof(args.summarize_trace, fd, wd, args.workload, args.bits,
+                          args.write_traffic)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this path runs on one GPU; figures for more than one GPU are not "

@@ -19,7 +19,9 @@
  *   - All argument checks run on the host before anything is launched, so a
  *     call that returns an error has written nothing.  Asynchronous device
  *     faults surface at the caller's next synchronisation.
- *   - Calls keep no global state; they are reentrant and thread-safe.
+ *   - The only global state is a per-device cache of the compute-unit count
+ *     (read once per device with hipDeviceGetAttribute, then reused; it
+ *     sizes the launch grid).  Calls are reentrant and thread-safe.
  *   - No C++ exception crosses this interface.
  */
 #ifndef FEWBIT_H

@@ -32,20 +32,26 @@ def weight(spec):
     raise ValueError(spec)
 
 
+# Activations with an even f' also get the symmetric fit of the Fig. 3
+# caption (bins of |x|, fit on [0, B]), keyed "<workload>/b<bits>/sym".
+SYMMETRIC = ("sigmoid", "tanh")
+
+
 def main():
     out = {}
     for name, w in WORKLOADS.items():
         for b in w.bits:
-            t0 = time.time()
-            F = O.fit(ACT[w.act], b, weight(w.fit), w.fit["n_grid"])
-            key = f"{name}/b{b}"
-            out[key] = {
-                "act": w.act, "bits": b, "symmetric": False, "weight": w.fit,
-                "s": [float(v).hex() for v in F.s],
-                "v": [float(v).hex() for v in F.v],
-                "loss": F.loss,
-            }
-            print(f"{key}: loss={F.loss:.6g} ({time.time() - t0:.1f}s)", flush=True)
+            for sym in ((False, True) if w.act in SYMMETRIC else (False,)):
+                t0 = time.time()
+                F = O.fit(ACT[w.act], b, weight(w.fit), w.fit["n_grid"], symmetric=sym)
+                key = f"{name}/b{b}" + ("/sym" if sym else "")
+                out[key] = {
+                    "act": w.act, "bits": b, "symmetric": sym, "weight": w.fit,
+                    "s": [float(v).hex() for v in F.s],
+                    "v": [float(v).hex() for v in F.v],
+                    "loss": F.loss,
+                }
+                print(f"{key}: loss={F.loss:.6g} ({time.time() - t0:.1f}s)", flush=True)
     with open(os.path.join(HERE, "tables.json"), "w") as fh:
         json.dump(out, fh, indent=1, sort_keys=True)
         fh.write("\n")

@@ -119,7 +119,8 @@ def run_case(key: str, dt: str, x_bits: np.ndarray, g_bits: np.ndarray, label: s
     print(f"[parity] {label or key} dt={dt} n={n} bits={bits}", flush=True)
     s = np.float32([float.fromhex(h) for h in spec["s"]])
     v = np.float32([float.fromhex(h) for h in spec["v"]])
-    y_ref, c_ref = O.fwd(OACT[spec["act"]], ODT[dt], bits, s, x_bits, threads=THREADS)
+    y_ref, c_ref = O.fwd(OACT[spec["act"]], ODT[dt], bits, s, x_bits,
+                         symmetric=bool(spec.get("symmetric")), threads=THREADS)
     gin_ref = O.bwd(ODT[dt], bits, v, g_bits, c_ref, threads=THREADS)
 
     x = upload(x_bits, dt)

@@ -69,8 +69,11 @@ def _oracle_weight(spec):
 def test_library_fit_matches_oracle_fit(key):
     spec = TABLES[key]
     w = spec["weight"]
-    T = P.fit_table(spec["act"], spec["bits"], P.Weight.from_spec(w), w["n_grid"])
-    F = O.fit(ORACLE_ACT[spec["act"]], spec["bits"], _oracle_weight(w), w["n_grid"])
+    sym = bool(spec["symmetric"])
+    T = P.fit_table(spec["act"], spec["bits"], P.Weight.from_spec(w), w["n_grid"], symmetric=sym)
+    F = O.fit(ORACLE_ACT[spec["act"]], spec["bits"], _oracle_weight(w), w["n_grid"],
+              symmetric=sym)
+    assert T.flags == (P.FLAG_SYMMETRIC if sym else 0)
     assert T.loss == pytest.approx(F.loss, rel=1e-9)
     s_lib = np.float32(T.s)
     same = np.array_equal(s_lib, F.s)

@@ -4,16 +4,17 @@ Bit-exact on packed codes and grad_in; y within 2e-6 abs + 1e-5 rel (fp32)
 or 1 ulp (fp16 / bf16).  Cases: all five workloads at full size (the sizes
 the benchmark runs, in its launch configuration), the same workloads cut to
 ragged lengths, an edge-size sweep over every dtype x bits x activation,
-special values, boundaries, in-place aliasing, a second stream, canaries
-past every output, and the autograd wrapper.
+special values, boundaries, the symmetric (|x|) tables of Sigmoid and Tanh,
+in-place aliasing, a second stream, canaries past every output, and the
+autograd wrapper.
 """
 import numpy as np
 import pytest
 
 import oracle as O
 import workloads as WL
-from parity import (OACT, ODT, THREADS, check_exact, check_y, download, download_codes,
-                    golden_table, run_case, upload)
+from parity import (OACT, ODT, TABLES, THREADS, check_exact, check_y, download,
+                    download_codes, golden_table, run_case, upload)
 
 pytestmark = pytest.mark.gpu
 
@@ -62,8 +63,8 @@ EDGE_N = [1, 2, 31, 32, 33, 63, 64, 65, 511, 512, 513, 1023, 1024, 1025, 4095, (
 
 def _synthetic_table(act, bits):
     import oracle as O
-    key = {"gelu": "cfg1_gelu3_f32_1M/b3", "silu": "cfg3_silu2_f16_resnet/b2",
-           "sigmoid": "cfg5_sigmoid4_f32_odd/b4", "tanh": "cfg5_tanh3_f32_odd/b3"}[act]
+    key = {"gelu": "gelu3_f32_1m/b3", "silu": "silu2_f16_resnet_64x256x56x56/b2",
+           "sigmoid": "sigmoid4_f32_odd_67108863/b4", "tanh": "tanh3_f32_odd_67108863/b3"}[act]
     spec, _ = golden_table(key)
     if spec["bits"] == bits:
         s = np.float32([float.fromhex(h) for h in spec["s"]])
@@ -148,6 +149,53 @@ def test_special_values_and_boundaries(act, dt):
     rng = np.random.default_rng(11)
     g = O.round_array(ODT[dt], rng.normal(0, 1, x.size))
     _run_synthetic(act, bits, dt, x, g, f"special {act}")
+
+
+# Symmetric tables (Fig. 3 caption: an even f' is fitted on [0, B] and the
+# bins apply to |x|), fitted by the oracle for the Sigmoid and Tanh inputs.
+SYM = sorted((k.split("/")[0], int(k.split("/")[1][1:])) for k in TABLES if k.endswith("/sym"))
+
+
+@pytest.mark.parametrize("name,bits", SYM, ids=[f"{n}-b{b}" for n, b in SYM])
+def test_symmetric_full_size(name, bits):
+    w = WL.WORKLOADS[name]
+    x, g = inputs(name)
+    print(run_case(f"{name}/b{bits}/sym", w.dtype, x, g, label=f"{name} b{bits} sym full"),
+          flush=True)
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("name,bits", SYM, ids=[f"{n}-b{b}" for n, b in SYM])
+def test_symmetric_half_types(name, bits, dt):
+    w = WL.WORKLOADS[name]
+    for n in (1, 513, 4097, (1 << 20) + 3):
+        x = WL.draw(w.x_dist, w.x_scale, n, dt, w.seed)
+        g = WL.draw("normal", w.g_sigma, n, dt, w.seed + 1000)
+        run_case(f"{name}/b{bits}/sym", dt, x, g, label=f"{name} b{bits} sym {dt} n={n}")
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("name,bits", SYM, ids=[f"{n}-b{b}" for n, b in SYM])
+def test_symmetric_special_values(name, bits, dt):
+    key = f"{name}/b{bits}/sym"
+    spec, _ = golden_table(key)
+    s = np.float32([float.fromhex(h) for h in spec["s"]])
+    xd = _special_values(dt, s)
+    x = O.round_array(ODT[dt], np.concatenate([xd, -xd]))
+    # +-boundary and its storage neighbours: |x| lands on, just below and
+    # just above every boundary from both sides of zero
+    if dt == "f32":
+        sb = s.view(np.uint32)
+        nb = np.concatenate([sb, sb + 1, sb - 1])
+        x = np.concatenate([x, nb, nb | np.uint32(0x80000000)])
+    else:
+        hb = O.round_array(ODT[dt], s.astype(np.float64))
+        nb = np.concatenate([hb, (hb + 1).astype(np.uint16), (hb - 1).astype(np.uint16)])
+        x = np.concatenate([x, nb, nb | np.uint16(0x8000)])
+    x = np.tile(x, 3)
+    rng = np.random.default_rng(13)
+    g = O.round_array(ODT[dt], rng.normal(0, 1, x.size))
+    run_case(key, dt, x, g, label=f"{key} special {dt}")
 
 
 def _canary_buffers(n, dt, bits):
