@@ -19,17 +19,16 @@
 // is reused), by a grid sized to the device's compute units so each wave
 // walks many tiles.
 //
-// Classification.  For fp16 / bf16 inputs every one of the 65536 input bit
-// patterns gets its interval index in a 64 KiB LDS table, built by each
-// workgroup from the boundaries before streaming (the index is monotone in
-// the value within a run of patterns that share sign and exponent, so the
-// table is filled run by run and checked at both ends of each 16-pattern
-// run; only runs holding a boundary, infinities or NaNs are evaluated one by
-// one).  A lookup then costs one LDS byte read instead of 2^b - 1 compares.
-// fp32 inputs compare against the boundaries held in scalar registers.
+// fp16 / bf16 forward.  Output pattern and interval index are functions of
+// the 16-bit input pattern alone, so each workgroup looks both up in LDS
+// tables over all 65536 patterns: the outputs (evaluated once per device by
+// a table kernel) and the indices (4 bits per pattern, built per launch from
+// the boundaries).  A lookup costs two LDS reads instead of an evaluation of
+// f and 2^b - 1 compares.  The fp32 forward evaluates f and compares against
+// the boundaries held in scalar registers.
 //
-// The table travels as kernel arguments (scalar registers); the backward
-// mirrors the values into LDS for per-lane lookup.
+// The fitted table travels as kernel arguments (scalar registers); the
+// backward mirrors its values into LDS for per-lane lookup.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -37,18 +36,20 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
+#include <mutex>
 
 #include "../../include/fewbit.h"
 
 // Launch-shape knobs (compile time): threads per workgroup, workgroups per
 // CU (the grid is capped at that many per compute unit and waves then walk
 // the tiles) and tiles in flight per wave, per kernel.  The fp16 / bf16
-// forward holds a 64 KiB table per workgroup, so at most 2 fit per CU.
+// forward holds 160 KiB of tables per workgroup (all of a CU's LDS), so one
+// workgroup fits per CU.
 #ifndef FEWBIT_FWD16_THREADS
 #define FEWBIT_FWD16_THREADS 512
 #endif
 #ifndef FEWBIT_FWD16_WG_PER_CU
-#define FEWBIT_FWD16_WG_PER_CU 2
+#define FEWBIT_FWD16_WG_PER_CU 1
 #endif
 #ifndef FEWBIT_FWD16_UNROLL
 #define FEWBIT_FWD16_UNROLL 4
@@ -300,30 +301,6 @@ __device__ inline uint32_t classify(float x, const TableArgs& tab) {
   return c;
 }
 
-// Interval index of every 16-bit input pattern, one byte each.
-template <int DT, int BITS>
-__device__ void build_code_table(uint8_t* lut, const TableArgs& tab, int symmetric) {
-  auto code_of = [&](uint32_t p) {
-    const float v = Half<DT>::widen(p);
-    return classify<BITS>(symmetric ? fabsf(v) : v, tab);
-  };
-  for (uint32_t run = threadIdx.x; run < 4096u; run += blockDim.x) {
-    const uint32_t p0 = run * 16u;
-    const uint32_t a = code_of(p0), b = code_of(p0 + 15u);
-    u32x4_t w;
-    if (!Half<DT>::special_run(p0) && a == b) {
-      const uint32_t rep = a * 0x01010101u;
-      w = (u32x4_t){rep, rep, rep, rep};
-    } else {
-      uint32_t q[4] = {0u, 0u, 0u, 0u};
-      for (uint32_t k = 0; k < 16u; ++k) q[k >> 2] |= code_of(p0 + k) << (8u * (k & 3u));
-      w = (u32x4_t){q[0], q[1], q[2], q[3]};
-    }
-    *reinterpret_cast<u32x4_t*>(lut + p0) = w;
-  }
-  __syncthreads();
-}
-
 // ---------------------------------------------------------------- packing
 // quad_perm DPP control: lane k of each quad reads lane sel[k] of the quad.
 constexpr int quad_perm(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
@@ -406,17 +383,103 @@ __device__ inline WaveIndex wave_index() {
 }
 
 // ---------------------------------------------------------------- forward, fp16 / bf16
-template <int DT, int BITS, int ACT>
-__device__ inline void fwd16_tile(u32x4_t in, const uint8_t* lut, u32x4_t& out, uint32_t& F) {
-  using H = Half<DT>;
+// For 16-bit inputs both results of the forward are functions of the input
+// bit pattern alone, so every workgroup holds two tables over all 65536
+// patterns in LDS:
+//   ylut  the output pattern of f(x), 128 KiB;
+//   clut  the interval index, 4 bits per pattern: byte q holds pattern 2q in
+//         its low and pattern 2q+1 in its high nibble, 32 KiB.
+// A tile then costs two LDS reads and a few integer operations per element
+// instead of an evaluation of f and the compares.
+//
+// ylut depends only on the activation and the storage type.  All eight
+// (activation, 16-bit type) tables are evaluated once per device by
+// output_tables_kernel (the f of the fp32 path, then one rounding to the
+// storage type) into a static device array, before the first fp16 / bf16
+// forward on that device; each workgroup copies the one it needs into LDS
+// with direct global-to-LDS loads.  clut depends on the boundaries and is
+// built by every workgroup: the index is monotone in the value within a run
+// of 16 patterns that share sign and exponent, so a run whose two ends agree
+// is filled without evaluating the rest; only runs holding a boundary,
+// infinities or NaNs are classified pattern by pattern.
+__device__ __attribute__((aligned(16))) uint16_t g_ytab[4][2][65536];
+
+template <int DT, int ACT>
+__device__ void fill_output_pair(uint32_t p) {
+  reinterpret_cast<uint32_t*>(g_ytab[ACT][DT - FEWBIT_F16])[p >> 1] =
+      Half<DT>::pack(Act<DT, ACT>::f(Half<DT>::widen(p)), Act<DT, ACT>::f(Half<DT>::widen(p + 1)));
+}
+
+// One thread per pair of patterns of one of the eight tables.
+constexpr uint32_t kTablePairs = 8u * 32768u;
+__global__ __launch_bounds__(256) void output_tables_kernel() {
+  const uint32_t gid = blockIdx.x * 256u + threadIdx.x;
+  if (gid >= kTablePairs) return;
+  const uint32_t p = (gid & 32767u) * 2u;
+  switch (gid >> 15) {
+    case 0: fill_output_pair<FEWBIT_F16, FEWBIT_GELU>(p); break;
+    case 1: fill_output_pair<FEWBIT_BF16, FEWBIT_GELU>(p); break;
+    case 2: fill_output_pair<FEWBIT_F16, FEWBIT_SILU>(p); break;
+    case 3: fill_output_pair<FEWBIT_BF16, FEWBIT_SILU>(p); break;
+    case 4: fill_output_pair<FEWBIT_F16, FEWBIT_SIGMOID>(p); break;
+    case 5: fill_output_pair<FEWBIT_BF16, FEWBIT_SIGMOID>(p); break;
+    case 6: fill_output_pair<FEWBIT_F16, FEWBIT_TANH>(p); break;
+    default: fill_output_pair<FEWBIT_BF16, FEWBIT_TANH>(p); break;
+  }
+}
+
+// ylut <- the device table of (ACT, DT), 1 KiB per wave instruction (lane l
+// moves bytes 16 l .. 16 l + 15 of the chunk).  The caller waits for the
+// loads and synchronises the workgroup before reading ylut.
+template <int DT, int ACT>
+__device__ void load_output_table(uint16_t* ylut) {
+  const uint8_t* src = reinterpret_cast<const uint8_t*>(g_ytab[ACT][DT - FEWBIT_F16]);
+  uint8_t* dst = reinterpret_cast<uint8_t*>(ylut);
+  const uint32_t lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  for (uint32_t c = wave; c < 128u; c += FEWBIT_FWD16_THREADS / kWave)
+    __builtin_amdgcn_global_load_lds(src + c * 1024u + lane * 16u,
+                                     (__attribute__((address_space(3))) void*)(dst + c * 1024u),
+                                     16, 0, 0);
+}
+
+template <int DT, int BITS>
+__device__ void build_code_table(uint8_t* clut, const TableArgs& tab, int symmetric) {
+  auto code_of = [&](uint32_t p) {
+    const float v = Half<DT>::widen(p);
+    return classify<BITS>(symmetric ? fabsf(v) : v, tab);
+  };
+  for (uint32_t run = threadIdx.x; run < 4096u; run += FEWBIT_FWD16_THREADS) {
+    const uint32_t p0 = run * 16u;
+    const uint32_t a = code_of(p0), b = code_of(p0 + 15u);
+    uint32_t q0, q1;
+    if (!Half<DT>::special_run(p0) && a == b) {
+      q0 = q1 = a * 0x11111111u;
+    } else {
+      q0 = q1 = 0u;
+      for (uint32_t k = 0; k < 8u; ++k) {
+        q0 |= code_of(p0 + k) << (4u * k);
+        q1 |= code_of(p0 + 8u + k) << (4u * k);
+      }
+    }
+    *reinterpret_cast<uint2*>(clut + run * 8u) = make_uint2(q0, q1);
+  }
+}
+
+__device__ inline uint32_t code_of_pattern(const uint8_t* clut, uint32_t p) {
+  return (static_cast<uint32_t>(clut[p >> 1]) >> ((p & 1u) << 2)) & 15u;
+}
+
+template <int BITS>
+__device__ inline void fwd16_tile(u32x4_t in, const uint16_t* ylut, const uint8_t* clut,
+                                  u32x4_t& out, uint32_t& F) {
   F = 0;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const uint32_t w = in[k];
-    const uint32_t c0 = lut[w & 0xFFFFu], c1 = lut[w >> 16];
-    const float y0 = Act<DT, ACT>::f(H::lo(w)), y1 = Act<DT, ACT>::f(H::hi(w));
-    out[k] = H::pack(y0, y1);
-    F |= (c0 << (2 * k * BITS)) | (c1 << ((2 * k + 1) * BITS));
+    const uint32_t lo = w & 0xFFFFu, hi = w >> 16;
+    out[k] = static_cast<uint32_t>(ylut[lo]) | (static_cast<uint32_t>(ylut[hi]) << 16);
+    F |= (code_of_pattern(clut, lo) << (2 * k * BITS)) |
+         (code_of_pattern(clut, hi) << ((2 * k + 1) * BITS));
   }
 }
 
@@ -426,8 +489,15 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
     TableArgs tab, int symmetric) {
   constexpr int U = FEWBIT_FWD16_UNROLL;
   constexpr int kWords = 16 * BITS;
-  __shared__ __attribute__((aligned(16))) uint8_t lut[65536];
-  build_code_table<DT, BITS>(lut, tab, symmetric);
+  // clut first: ylut's 32 KiB offset then fits the LDS instruction's
+  // immediate offset field
+  __shared__ __attribute__((aligned(16))) uint8_t tables[32768 + 2 * 65536];
+  uint8_t* clut = tables;
+  uint16_t* ylut = reinterpret_cast<uint16_t*>(tables + 32768);
+  load_output_table<DT, ACT>(ylut);
+  build_code_table<DT, BITS>(clut, tab, symmetric);
+  __builtin_amdgcn_s_waitcnt(0);     // the table loads have landed in LDS
+  __syncthreads();
 
   const WaveIndex wi = wave_index();
   const int64_t full = n / kTile;
@@ -441,7 +511,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (t0 + u) * kTile + lane_off);
 #pragma unroll
-    for (int u = 0; u < U; ++u) fwd16_tile<DT, BITS, ACT>(in[u], lut, out[u], F[u]);
+    for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
@@ -451,7 +521,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
     u32x4_t out;
     uint32_t F;
-    fwd16_tile<DT, BITS, ACT>(ld_stream(x + t * kTile + lane_off), lut, out, F);
+    fwd16_tile<BITS>(ld_stream(x + t * kTile + lane_off), ylut, clut, out, F);
     st_stream(y + t * kTile + lane_off, out);
     pack_store<BITS>(codes + t * kWords, F, wi.lane, kWords);
   }
@@ -463,9 +533,9 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
     for (int j = 0; j < kPerLane; ++j) {
       const int64_t e = t * kTile + lane_off + j;
       if (e < n) {
-        const uint32_t bits16 = x[e];
-        Scalar<DT>::store(y, e, Act<DT, ACT>::f(Half<DT>::widen(bits16)));
-        F |= static_cast<uint32_t>(lut[bits16]) << (BITS * j);
+        const uint32_t p = x[e];
+        y[e] = ylut[p];
+        F |= code_of_pattern(clut, p) << (BITS * j);
       }
     }
     const int64_t wbase = t * kWords;
@@ -705,6 +775,37 @@ dim3 grid_for(int64_t n, int threads, int wg_per_cu) {
   return dim3(static_cast<unsigned>(blocks));
 }
 
+// The output tables of the fp16 / bf16 forward, once per device: evaluated
+// on a private non-blocking stream that the host waits for, so that every
+// later launch on any stream reads complete tables.  Thread-safe.
+int ensure_output_tables() {
+  static std::atomic<int> ready[64];
+  static std::mutex mu;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return FEWBIT_E_HIP;
+  if (ready[dev].load(std::memory_order_acquire)) return FEWBIT_OK;
+  std::lock_guard<std::mutex> lock(mu);
+  if (ready[dev].load(std::memory_order_relaxed)) return FEWBIT_OK;
+  hipStream_t s = nullptr;
+  hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+  if (e == hipSuccess) {
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(output_tables_kernel, dim3(kTablePairs / 256u), dim3(256), 0, s);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    const hipError_t d = hipStreamDestroy(s);
+    if (e == hipSuccess) e = d;
+  }
+  if (e != hipSuccess) {
+    if (std::getenv("FEWBIT_DEBUG"))
+      std::fprintf(stderr, "fewbit: output tables: %s (%s)\n", hipGetErrorName(e),
+                   hipGetErrorString(e));
+    return FEWBIT_E_HIP;
+  }
+  ready[dev].store(1, std::memory_order_release);
+  return FEWBIT_OK;
+}
+
 struct Launch {
   const fewbit_table* t;
   const void* in;
@@ -795,6 +896,10 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   if (n == 0) return FEWBIT_OK;
   if (!x || !y || !codes) return FEWBIT_E_NULL;
   if (misaligned(x) || misaligned(y) || misaligned(codes)) return FEWBIT_E_ALIGN;
+  if (dtype != FEWBIT_F32) {
+    rc = ensure_output_tables();
+    if (rc != FEWBIT_OK) return rc;
+  }
   const Launch L{t, x, y, codes, n, static_cast<hipStream_t>(stream)};
   switch (dtype) {
     case FEWBIT_F32: launch_fwd_bits<FEWBIT_F32>(L); break;
