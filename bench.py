@@ -67,7 +67,8 @@ def _kernel_key(name: str):
     import re
     m = re.search(r"(fwd16_kernel|fwd32_kernel|bwd_kernel)<([0-9, ]+)>", name)
     if not m:
-        return name.split("(")[0]
+        base = name.replace("(anonymous namespace)::", "").replace("void ", "")
+        return base.split("(")[0].strip() or name
     args = [int(a) for a in m.group(2).split(",")]
     if m.group(1) == "fwd16_kernel":
         return f"fwd16_kernel<{DT_NAMES[args[0]]},{args[1]},{ACT_NAMES[args[2]]}>"
@@ -108,11 +109,16 @@ def summarize_rocprof(trace_dir, fetch_dir, write_dir, workload, bits, out_traff
         for r in _csv(_one(trace_dir, "kernel_stats.csv")):
             key = _kernel_key(r["Name"])
             avg = float(r["AverageNs"]) / 1e3
-            is_lib = key.startswith(("fwd", "bwd"))
-            b = alg if is_lib else 2 * copy_bytes
-            gbps = b / (avg * 1e-6) / 1e9
+            if key.startswith(("fwd", "bwd")):
+                b = alg
+            elif "copyBuffer" in key:
+                b = 2 * copy_bytes
+            else:
+                b = None            # not a streaming kernel of this workload
+            rate = (f"{b / (avg * 1e-6) / 1e9:10.1f} {b / (avg * 1e-6) / 1e9 / HBM_PEAK_GBPS:10.4f}"
+                    if b else f"{'-':>10s} {'-':>10s}")
             lines.append(f"{key:34s} {int(r['Calls']):6d} {avg:9.2f} {float(r['MinNs']) / 1e3:10.2f} "
-                         f"{float(r['MaxNs']) / 1e3:10.2f} {gbps:10.1f} {gbps / HBM_PEAK_GBPS:10.4f}")
+                         f"{float(r['MaxNs']) / 1e3:10.2f} {rate}")
     traffic = {}
     if fetch_dir and write_dir:
         per = {}

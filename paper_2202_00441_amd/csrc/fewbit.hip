@@ -119,7 +119,9 @@ struct Half<FEWBIT_BF16> {
   __device__ static uint32_t pack(float a, float b) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
   }
+  // runs of 16 patterns with the exponent all ones: infinity, then NaNs
   __device__ static bool special_run(uint32_t p) { return (p & 0x7F80u) == 0x7F80u; }
+  static constexpr uint32_t kMantissa = 0x7Fu;
 };
 
 template <>
@@ -137,6 +139,7 @@ struct Half<FEWBIT_F16> {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, f16x2_t));
   }
   __device__ static bool special_run(uint32_t p) { return (p & 0x7C00u) == 0x7C00u; }
+  static constexpr uint32_t kMantissa = 0x3FFu;
 };
 
 // element-wise access for the partial tile at the end
@@ -400,8 +403,9 @@ __device__ inline WaveIndex wave_index() {
 // with direct global-to-LDS loads.  clut depends on the boundaries and is
 // built by every workgroup: the index is monotone in the value within a run
 // of 16 patterns that share sign and exponent, so a run whose two ends agree
-// is filled without evaluating the rest; only runs holding a boundary,
-// infinities or NaNs are classified pattern by pattern.
+// is filled without evaluating the rest, and the runs of infinities and
+// NaNs by rule (an infinity opens its run, every NaN takes index 0); only
+// runs holding a boundary are classified pattern by pattern.
 __device__ __attribute__((aligned(16))) uint16_t g_ytab[4][2][65536];
 
 template <int DT, int ACT>
@@ -452,7 +456,11 @@ __device__ void build_code_table(uint8_t* clut, const TableArgs& tab, int symmet
     const uint32_t p0 = run * 16u;
     const uint32_t a = code_of(p0), b = code_of(p0 + 15u);
     uint32_t q0, q1;
-    if (!Half<DT>::special_run(p0) && a == b) {
+    if (Half<DT>::special_run(p0)) {
+      // an infinity opens the first such run (its index is a); NaNs take 0
+      q0 = ((p0 & Half<DT>::kMantissa) == 0u) ? a : 0u;
+      q1 = 0u;
+    } else if (a == b) {
       q0 = q1 = a * 0x11111111u;
     } else {
       q0 = q1 = 0u;
