@@ -15,13 +15,18 @@
  *   - Plain C types only.  Device pointers are HIP device addresses; the
  *     stream argument is a hipStream_t passed as void* (NULL = null stream).
  *   - The caller owns every buffer.  The library never allocates or frees
- *     device memory and never synchronises the device.
+ *     device memory and never synchronises the caller's streams.
  *   - All argument checks run on the host before anything is launched, so a
  *     call that returns an error has written nothing.  Asynchronous device
  *     faults surface at the caller's next synchronisation.
- *   - The only global state is a per-device cache of the compute-unit count
- *     (read once per device with hipDeviceGetAttribute, then reused; it
- *     sizes the launch grid).  Calls are reentrant and thread-safe.
+ *   - Global state, per device: the compute-unit count (read once, it sizes
+ *     the launch grid) and, for the fp16 / bf16 forward, static device
+ *     tables of f over all 65536 input patterns of each activation and
+ *     type (1.75 MiB of module memory).  The first fp16 / bf16 fewbit_fwd on
+ *     a device evaluates those tables on a private non-blocking stream and
+ *     waits for that stream alone; it therefore must not be made while a
+ *     stream is being captured into a graph in a mode that forbids
+ *     synchronisation.  Calls are reentrant and thread-safe.
  *   - No C++ exception crosses this interface.
  */
 #ifndef FEWBIT_H
@@ -46,11 +51,16 @@ extern "C" {
 #define FEWBIT_E_NUMERIC   -7  /* table not strictly sorted / not finite   */
 #define FEWBIT_E_HIP       -8  /* a HIP launch or runtime call failed      */
 
-/* Activations (Table 1 rows in scope; Swish is x*sigmoid(x), Sec. 4). */
+/* Activations: the rows of Table 1 (Swish is x*sigmoid(x), Sec. 4). */
 #define FEWBIT_GELU     0      /* x * Phi(x), Phi the standard normal cdf  */
 #define FEWBIT_SILU     1      /* x * sigmoid(x)                           */
 #define FEWBIT_SIGMOID  2      /* 1 / (1 + exp(-x))                        */
 #define FEWBIT_TANH     3      /* tanh(x)                                  */
+#define FEWBIT_RELU     4      /* max(x, 0); f' = 1 for x > 0, else 0      */
+#define FEWBIT_SELU     5      /* lambda x (x > 0), lambda alpha (e^x - 1)
+                                  (x <= 0), lambda = 1.0507009873554805,
+                                  alpha = 1.6732632423543772              */
+#define FEWBIT_SOFTPLUS 6      /* log(1 + e^x)                             */
 
 /* Storage types of x, y, grad_out, grad_in. */
 #define FEWBIT_F32   0         /* IEEE binary32                            */
@@ -86,7 +96,7 @@ typedef struct fewbit_weight {
  * call, so it may be reused or freed as soon as the call returns.
  */
 typedef struct fewbit_table {
-    int32_t act;           /* FEWBIT_GELU .. FEWBIT_TANH                   */
+    int32_t act;           /* FEWBIT_GELU .. FEWBIT_SOFTPLUS               */
     int32_t bits;          /* 1..4                                         */
     int32_t flags;         /* 0 or FEWBIT_FLAG_SYMMETRIC                   */
     int32_t reserved;      /* must be 0                                    */

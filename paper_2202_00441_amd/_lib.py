@@ -18,12 +18,13 @@ LIB_PATH = os.path.join(HERE, "libfewbit.so")
 # status codes, activations, storage types, weights, flags (include/fewbit.h)
 OK, E_INVALID, E_NULL, E_ALIGN, E_DTYPE, E_BITS, E_NOMEM, E_NUMERIC, E_HIP = \
     0, -1, -2, -3, -4, -5, -6, -7, -8
-GELU, SILU, SIGMOID, TANH = 0, 1, 2, 3
+GELU, SILU, SIGMOID, TANH, RELU, SELU, SOFTPLUS = 0, 1, 2, 3, 4, 5, 6
 F32, F16, BF16 = 0, 1, 2
 W_UNIFORM, W_NORMAL, W_MIXTURE = 0, 1, 2
 FLAG_SYMMETRIC = 1
 
-ACTS = {"gelu": GELU, "silu": SILU, "swish": SILU, "sigmoid": SIGMOID, "tanh": TANH}
+ACTS = {"gelu": GELU, "silu": SILU, "swish": SILU, "sigmoid": SIGMOID, "tanh": TANH,
+        "relu": RELU, "selu": SELU, "softplus": SOFTPLUS}
 DTYPES = {"f32": F32, "f16": F16, "bf16": BF16}
 
 

@@ -24,7 +24,7 @@ class FewBitActivation(torch.autograd.Function):
 
 
 class FewBitAct(torch.nn.Module):
-    """Few-bit GELU / SiLU / Sigmoid / Tanh.
+    """Few-bit GELU / SiLU / Sigmoid / Tanh / ReLU / SELU / Softplus.
 
     The table is fitted once at construction (Sec. 3); by default under a
     standard normal weight on [-10, 10] with a 4000-cell grid.

@@ -135,7 +135,12 @@ struct Half<FEWBIT_F16> {
   __device__ static float widen(uint32_t bits16) {
     return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
   }
+  // Round to nearest even from the fp32 value.  The operands pass an empty
+  // register barrier first: without it the compiler may fuse the multiply
+  // or FMA that produced them into one mixed-precision FMA rounded straight
+  // to fp16, which rounds once instead of twice and turns -0 into +0.
   __device__ static uint32_t pack(float a, float b) {
+    asm("" : "+v"(a), "+v"(b));
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, f16x2_t));
   }
   __device__ static bool special_run(uint32_t p) { return (p & 0x7C00u) == 0x7C00u; }
@@ -293,6 +298,29 @@ struct Act<DT, FEWBIT_TANH> {
   __device__ static float f(float x) { return tanhf(x); }
 };
 
+template <int DT>
+struct Act<DT, FEWBIT_RELU> {
+  // +0 for every x <= 0, NaN kept
+  __device__ static float f(float x) { return x > 0.0f ? x : (x == x ? 0.0f : x); }
+};
+
+// Klambauer et al. (2017): lambda and lambda * alpha
+constexpr float kSeluLambda = 1.0507009873554805f;
+constexpr float kSeluLambdaAlpha = 1.7580993408473766f;
+
+template <int DT>
+struct Act<DT, FEWBIT_SELU> {
+  __device__ static float f(float x) {
+    return x > 0.0f ? kSeluLambda * x : kSeluLambdaAlpha * expm1f(x);   // NaN via expm1f
+  }
+};
+
+template <int DT>
+struct Act<DT, FEWBIT_SOFTPLUS> {
+  // max(x, 0) + log(1 + e^-|x|): no overflow, full accuracy in both tails
+  __device__ static float f(float x) { return relu(x) + log1pf(expf(-fabsf(x))); }
+};
+
 // ---------------------------------------------------------------- classify
 // idx = number of boundaries s[m] <= x: half-open intervals [s[m-1], s[m]).
 // IEEE compares: NaN gives 0, -0 == +0, subnormals are not flushed.
@@ -395,7 +423,7 @@ __device__ inline WaveIndex wave_index() {
 // A tile then costs two LDS reads and a few integer operations per element
 // instead of an evaluation of f and the compares.
 //
-// ylut depends only on the activation and the storage type.  All eight
+// ylut depends only on the activation and the storage type.  All
 // (activation, 16-bit type) tables are evaluated once per device by
 // output_tables_kernel (the f of the fp32 path, then one rounding to the
 // storage type) into a static device array, before the first fp16 / bf16
@@ -406,7 +434,8 @@ __device__ inline WaveIndex wave_index() {
 // is filled without evaluating the rest, and the runs of infinities and
 // NaNs by rule (an infinity opens its run, every NaN takes index 0); only
 // runs holding a boundary are classified pattern by pattern.
-__device__ __attribute__((aligned(16))) uint16_t g_ytab[4][2][65536];
+constexpr int kActs = FEWBIT_SOFTPLUS + 1;
+__device__ __attribute__((aligned(16))) uint16_t g_ytab[kActs][2][65536];
 
 template <int DT, int ACT>
 __device__ void fill_output_pair(uint32_t p) {
@@ -414,21 +443,28 @@ __device__ void fill_output_pair(uint32_t p) {
       Half<DT>::pack(Act<DT, ACT>::f(Half<DT>::widen(p)), Act<DT, ACT>::f(Half<DT>::widen(p + 1)));
 }
 
-// One thread per pair of patterns of one of the eight tables.
-constexpr uint32_t kTablePairs = 8u * 32768u;
+// One thread per pair of patterns of one of the tables.
+constexpr uint32_t kTablePairs = 2u * kActs * 32768u;
+
+template <int ACT>
+__device__ void fill_output_pair_act(uint32_t dt, uint32_t p) {
+  if (dt == 0) fill_output_pair<FEWBIT_F16, ACT>(p);
+  else fill_output_pair<FEWBIT_BF16, ACT>(p);
+}
+
 __global__ __launch_bounds__(256) void output_tables_kernel() {
   const uint32_t gid = blockIdx.x * 256u + threadIdx.x;
   if (gid >= kTablePairs) return;
   const uint32_t p = (gid & 32767u) * 2u;
-  switch (gid >> 15) {
-    case 0: fill_output_pair<FEWBIT_F16, FEWBIT_GELU>(p); break;
-    case 1: fill_output_pair<FEWBIT_BF16, FEWBIT_GELU>(p); break;
-    case 2: fill_output_pair<FEWBIT_F16, FEWBIT_SILU>(p); break;
-    case 3: fill_output_pair<FEWBIT_BF16, FEWBIT_SILU>(p); break;
-    case 4: fill_output_pair<FEWBIT_F16, FEWBIT_SIGMOID>(p); break;
-    case 5: fill_output_pair<FEWBIT_BF16, FEWBIT_SIGMOID>(p); break;
-    case 6: fill_output_pair<FEWBIT_F16, FEWBIT_TANH>(p); break;
-    default: fill_output_pair<FEWBIT_BF16, FEWBIT_TANH>(p); break;
+  const uint32_t table = gid >> 15, dt = table & 1u;
+  switch (table >> 1) {
+    case FEWBIT_GELU: fill_output_pair_act<FEWBIT_GELU>(dt, p); break;
+    case FEWBIT_SILU: fill_output_pair_act<FEWBIT_SILU>(dt, p); break;
+    case FEWBIT_SIGMOID: fill_output_pair_act<FEWBIT_SIGMOID>(dt, p); break;
+    case FEWBIT_TANH: fill_output_pair_act<FEWBIT_TANH>(dt, p); break;
+    case FEWBIT_RELU: fill_output_pair_act<FEWBIT_RELU>(dt, p); break;
+    case FEWBIT_SELU: fill_output_pair_act<FEWBIT_SELU>(dt, p); break;
+    default: fill_output_pair_act<FEWBIT_SOFTPLUS>(dt, p); break;
   }
 }
 
@@ -732,7 +768,7 @@ __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
 int check_table(const fewbit_table* t) {
   if (!t) return FEWBIT_E_NULL;
   if (t->bits < 1 || t->bits > 4) return FEWBIT_E_BITS;
-  if (t->act < FEWBIT_GELU || t->act > FEWBIT_TANH) return FEWBIT_E_INVALID;
+  if (t->act < FEWBIT_GELU || t->act > FEWBIT_SOFTPLUS) return FEWBIT_E_INVALID;
   if ((t->flags & ~FEWBIT_FLAG_SYMMETRIC) != 0 || t->reserved != 0) return FEWBIT_E_INVALID;
   const int K = 1 << t->bits;
   for (int m = 0; m < K - 1; ++m) {
@@ -848,7 +884,10 @@ void launch_fwd_act(const Launch& L) {
     case FEWBIT_GELU: launch_fwd<DT, BITS, FEWBIT_GELU>(L); break;
     case FEWBIT_SILU: launch_fwd<DT, BITS, FEWBIT_SILU>(L); break;
     case FEWBIT_SIGMOID: launch_fwd<DT, BITS, FEWBIT_SIGMOID>(L); break;
-    default: launch_fwd<DT, BITS, FEWBIT_TANH>(L); break;
+    case FEWBIT_TANH: launch_fwd<DT, BITS, FEWBIT_TANH>(L); break;
+    case FEWBIT_RELU: launch_fwd<DT, BITS, FEWBIT_RELU>(L); break;
+    case FEWBIT_SELU: launch_fwd<DT, BITS, FEWBIT_SELU>(L); break;
+    default: launch_fwd<DT, BITS, FEWBIT_SOFTPLUS>(L); break;
   }
 }
 

@@ -28,7 +28,7 @@ namespace {
 
 constexpr double kPi = 3.141592653589793238462643383279502884;
 
-// --- derivatives of the in-scope activations, in double -------------------
+// --- derivatives of the activations, in double ----------------------------
 double logistic(double x) {
   // evaluated on the side where exp() cannot overflow
   if (x < 0.0) {
@@ -58,6 +58,16 @@ double activation_derivative(int act, double x) {
       const double th = std::tanh(x);
       return (1.0 - th) * (1.0 + th);
     }
+    case FEWBIT_RELU:
+      return x > 0.0 ? 1.0 : 0.0;
+    case FEWBIT_SELU: {
+      // Klambauer et al. (2017): lambda and lambda * alpha
+      constexpr double kLambda = 1.0507009873554804934;
+      constexpr double kLambdaAlpha = 1.7580993408473768600;
+      return x > 0.0 ? kLambda : kLambdaAlpha * std::exp(x);
+    }
+    case FEWBIT_SOFTPLUS:
+      return logistic(x);
   }
   return 0.0;
 }
@@ -118,7 +128,7 @@ extern "C" int fewbit_fit_table(int32_t act, int32_t bits, const fewbit_weight* 
                                 int64_t n_grid, int32_t flags, fewbit_table* out) {
   if (!w || !out) return FEWBIT_E_NULL;
   if (bits < 1 || bits > 4) return FEWBIT_E_BITS;
-  if (act < FEWBIT_GELU || act > FEWBIT_TANH) return FEWBIT_E_INVALID;
+  if (act < FEWBIT_GELU || act > FEWBIT_SOFTPLUS) return FEWBIT_E_INVALID;
   if (flags & ~FEWBIT_FLAG_SYMMETRIC) return FEWBIT_E_INVALID;
   if (w->reserved != 0) return FEWBIT_E_INVALID;
   if (w->kind < FEWBIT_W_UNIFORM || w->kind > FEWBIT_W_MIXTURE) return FEWBIT_E_INVALID;

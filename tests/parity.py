@@ -20,7 +20,8 @@ import oracle as O
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 TABLES = json.load(open(os.path.join(ROOT, "tests", "golden", "tables.json")))
 ODT = {"f32": O.F32, "f16": O.F16, "bf16": O.BF16}
-OACT = {"gelu": O.GELU, "silu": O.SILU, "sigmoid": O.SIGMOID, "tanh": O.TANH}
+OACT = {"gelu": O.GELU, "silu": O.SILU, "sigmoid": O.SIGMOID, "tanh": O.TANH,
+        "relu": O.RELU, "selu": O.SELU, "softplus": O.SOFTPLUS}
 THREADS = max(1, min(16, os.cpu_count() or 1))
 
 
@@ -106,7 +107,9 @@ def check_y(got: np.ndarray, ref: np.ndarray, dt: str, what: str = "y") -> dict:
 def check_exact(got: np.ndarray, ref: np.ndarray, what: str):
     assert got.shape == ref.shape, (what, got.shape, ref.shape)
     bad = np.flatnonzero(got != ref)
-    assert bad.size == 0, f"{what}: {bad.size} mismatches, first at {bad[:8]}"
+    assert bad.size == 0, (f"{what}: {bad.size} mismatches, first at {bad[:8]}: got "
+                           f"{[hex(int(v)) for v in got[bad[:4]]]} ref "
+                           f"{[hex(int(v)) for v in ref[bad[:4]]]}")
 
 
 def run_case(key: str, dt: str, x_bits: np.ndarray, g_bits: np.ndarray, label: str = ""):

@@ -54,7 +54,8 @@ def test_strerror():
     assert P.strerror(-99) == "unknown status"
 
 
-ORACLE_ACT = {"gelu": O.GELU, "silu": O.SILU, "sigmoid": O.SIGMOID, "tanh": O.TANH}
+ORACLE_ACT = {"gelu": O.GELU, "silu": O.SILU, "sigmoid": O.SIGMOID, "tanh": O.TANH,
+              "relu": O.RELU, "selu": O.SELU, "softplus": O.SOFTPLUS}
 
 
 def _oracle_weight(spec):
@@ -98,6 +99,47 @@ def test_library_fit_other_cases(act, bits, sym):
     assert T.loss == pytest.approx(F.loss, rel=1e-9)
     assert T.flags == (P.FLAG_SYMMETRIC if sym else 0)
     assert np.array_equal(np.float32(T.s), F.s) or np.array_equal(np.float32(T.s), -F.s[::-1])
+
+
+@pytest.mark.parametrize("act,bits", [(a, b) for a in ("relu", "selu", "softplus")
+                                      for b in (1, 2, 3, 4)])
+def test_library_fit_more_activations(act, bits):
+    w = P.Weight(P.W_UNIFORM, -10.0, 10.0)
+    T = P.fit_table(act, bits, w, 1000)
+    F = O.fit(ORACLE_ACT[act], bits, O.uniform(-10.0, 10.0), 1000)
+    assert T.loss == pytest.approx(F.loss, rel=1e-9, abs=1e-12)
+    assert np.all(np.diff(np.float32(T.s)) > 0)
+
+
+def _paper_table1():
+    rows = []
+    with open(os.path.join(os.path.dirname(__file__), "golden", "table1_fit_errors.txt")) as fh:
+        for line in fh:
+            if line.startswith("#") or not line.strip():
+                continue
+            name, sym, *vals = line.split()
+            for b, v in enumerate(vals, start=1):
+                if v != "-":
+                    rows.append((name, sym == "1", b, float(v)))
+    return rows
+
+
+@pytest.mark.parametrize("name,symmetric,bits,paper", _paper_table1())
+def test_library_fit_reproduces_table1(name, symmetric, bits, paper):
+    """The library's own fit (independent of the oracle) against the fit
+    errors the paper prints in Table 1 (4 decimals): w = 1 on [-10, 10]."""
+    act = "silu" if name == "swish" else name
+    T = P.fit_table(act, bits, P.Weight(P.W_UNIFORM, -10.0, 10.0), 4000, symmetric=symmetric)
+    assert abs(T.loss - paper) <= 1.01e-4, (T.loss, paper)
+
+
+def test_parity_helpers_cover_every_activation():
+    # the GPU parity helpers name the oracle's activation for every library one
+    from parity import OACT
+    for name, code in P.ACTS.items():
+        if name == "swish":
+            continue
+        assert OACT[name] == code == ORACLE_ACT[name]
 
 
 def test_fit_argument_errors():

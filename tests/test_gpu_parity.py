@@ -4,7 +4,8 @@ Bit-exact on packed codes and grad_in; y within 2e-6 abs + 1e-5 rel (fp32)
 or 1 ulp (fp16 / bf16).  Cases: all five workloads at full size (the sizes
 the benchmark runs, in its launch configuration), the same workloads cut to
 ragged lengths, an edge-size sweep over every dtype x bits x activation,
-special values, boundaries, the symmetric (|x|) tables of Sigmoid and Tanh,
+special values, boundaries, ReLU / SELU / Softplus (Table 1's other rows),
+the symmetric (|x|) tables of Sigmoid and Tanh,
 in-place aliasing, a second stream, canaries past every output, and the
 autograd wrapper.
 """
@@ -64,9 +65,9 @@ EDGE_N = [1, 2, 31, 32, 33, 63, 64, 65, 511, 512, 513, 1023, 1024, 1025, 4095, (
 def _synthetic_table(act, bits):
     import oracle as O
     key = {"gelu": "gelu3_f32_1m/b3", "silu": "silu2_f16_resnet_64x256x56x56/b2",
-           "sigmoid": "sigmoid4_f32_odd_67108863/b4", "tanh": "tanh3_f32_odd_67108863/b3"}[act]
-    spec, _ = golden_table(key)
-    if spec["bits"] == bits:
+           "sigmoid": "sigmoid4_f32_odd_67108863/b4", "tanh": "tanh3_f32_odd_67108863/b3"}.get(act)
+    spec = golden_table(key)[0] if key else None
+    if spec is not None and spec["bits"] == bits:
         s = np.float32([float.fromhex(h) for h in spec["s"]])
         v = np.float32([float.fromhex(h) for h in spec["v"]])
     else:
@@ -100,7 +101,10 @@ def test_edge_sizes_gelu(dt, bits):
         _run_synthetic("gelu", bits, dt, x, g, f"edge n={n}")
 
 
-@pytest.mark.parametrize("act", ["silu", "sigmoid", "tanh"])
+MORE_ACTS = ["relu", "selu", "softplus"]
+
+
+@pytest.mark.parametrize("act", ["silu", "sigmoid", "tanh"] + MORE_ACTS)
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_edge_sizes_other_acts(act, dt):
     rng = np.random.default_rng(7)
@@ -109,6 +113,17 @@ def test_edge_sizes_other_acts(act, dt):
             x = O.round_array(ODT[dt], rng.uniform(-9, 9, n))
             g = O.round_array(ODT[dt], rng.normal(0, 1, n))
             _run_synthetic(act, bits, dt, x, g, f"{act} n={n}")
+
+
+@pytest.mark.parametrize("act", MORE_ACTS)
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_more_activations_several_waves(act, dt):
+    # enough tiles for every wave of the grid to walk several, plus a ragged end
+    rng = np.random.default_rng(21)
+    n = (1 << 22) + 13
+    x = O.round_array(ODT[dt], rng.uniform(-9, 9, n))
+    g = O.round_array(ODT[dt], rng.normal(0, 1, n))
+    _run_synthetic(act, 2, dt, x, g, f"{act} n={n}")
 
 
 def _special_values(dt, s):
@@ -129,7 +144,7 @@ def _special_values(dt, s):
     return np.array(vals, np.float64)
 
 
-@pytest.mark.parametrize("act", ["gelu", "silu", "sigmoid", "tanh"])
+@pytest.mark.parametrize("act", ["gelu", "silu", "sigmoid", "tanh"] + MORE_ACTS)
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_special_values_and_boundaries(act, dt):
     bits = 3
