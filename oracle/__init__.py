@@ -86,6 +86,11 @@ def lib():
         L.oracle_prefix.argtypes = [i32, C.POINTER(_Weight), i64, vp, vp, vp]
         L.oracle_interval_cost.restype = d
         L.oracle_interval_cost.argtypes = [vp, vp, vp, i64, i64, i32, d, d]
+        L.oracle_loss_at.restype = i32
+        L.oracle_loss_at.argtypes = [i32, i32, C.POINTER(_Weight), i64, i32, vp, vp, vp, vp]
+        L.oracle_fit_refined.restype = i32
+        L.oracle_fit_refined.argtypes = [i32, i32, C.POINTER(_Weight), i64, i32, i32, vp, vp,
+                                         vp, vp, vp, vp, vp]
         L.oracle_fit.restype = i32
         L.oracle_fit.argtypes = [i32, i32, C.POINTER(_Weight), i64, i32, vp, vp,
                                  C.POINTER(d), vp, vp, vp]
@@ -217,6 +222,56 @@ def fit(act: int, bits: int, w: Weight, n: int, symmetric: bool = False) -> Fit:
     if rc != 0:
         raise ValueError(f"oracle_fit failed rc={rc}")
     return Fit(act, bits, symmetric, s, v, loss.value, cuts, dpl, vd)
+
+
+def loss_at(act: int, bits: int, w: Weight, n: int, s, symmetric: bool = False):
+    """(L, y, dL/ds) of Eq. (3) at interior boundaries s (double), Sec. 3."""
+    K = 1 << bits
+    sd = np.ascontiguousarray(s, dtype=np.float64)
+    assert sd.size == K - 1
+    y = np.zeros(K)
+    g = np.zeros(K - 1)
+    loss = C.c_double(0.0)
+    cw = w._c()
+    rc = lib().oracle_loss_at(act, bits, C.byref(cw), n, int(symmetric), _ptr(sd), _ptr(y),
+                              _ptr(g), C.byref(loss))
+    if rc != 0:
+        raise ValueError(f"oracle_loss_at failed rc={rc}")
+    return loss.value, y, g
+
+
+@dataclass
+class RefinedFit:
+    act: int
+    bits: int
+    symmetric: bool
+    s: np.ndarray        # fp32 boundaries after refinement
+    v: np.ndarray        # fp32 values
+    s_double: np.ndarray
+    v_double: np.ndarray
+    loss: float          # L after refinement (doubled for the symmetric fit)
+    loss_dp: float       # L of the DP starting point
+    iters: int
+
+
+def fit_refined(act: int, bits: int, w: Weight, n: int, symmetric: bool = False,
+                max_iter: int = 5000) -> RefinedFit:
+    """The DP fit, then gradient descent on the boundaries (Sec. 3)."""
+    K = 1 << bits
+    s = np.zeros(K - 1, np.float32)
+    v = np.zeros(K, np.float32)
+    sd = np.zeros(K - 1)
+    vd = np.zeros(K)
+    loss = C.c_double(0.0)
+    loss_dp = C.c_double(0.0)
+    iters = C.c_int(0)
+    cw = w._c()
+    rc = lib().oracle_fit_refined(act, bits, C.byref(cw), n, int(symmetric), max_iter, _ptr(s),
+                                  _ptr(v), _ptr(sd), _ptr(vd), C.byref(loss), C.byref(loss_dp),
+                                  C.byref(iters))
+    if rc != 0:
+        raise ValueError(f"oracle_fit_refined failed rc={rc}")
+    return RefinedFit(act, bits, symmetric, s, v, sd, vd, loss.value, loss_dp.value, iters.value)
 
 
 # ---------------------------------------------------------------- codes

@@ -33,6 +33,9 @@
  *                             as a dense little-endian LSB-first bit stream.
  *   backward               -- Eq. (1) with f' replaced by the stored value
  *                             y[idx] (Listing 1, backward).
+ *   refinement             -- Sec. 3: y(s) by Eq. (4), the analytic gradient
+ *                             of L(s, y(s)) in s, gradient descent from the
+ *                             DP result (reading R9).
  *
  * Readings where the paper is silent or garbled (each one is listed in the
  * design notes of the repository):
@@ -54,6 +57,10 @@
  *       boundaries s_m <= x.  NaN compares false (idx 0); -0 == +0.
  *   R8  Half-precision gradients are rounded twice by definition: the fp32
  *       product widen(g)*v[idx], then round-to-nearest-even to the dtype.
+ *   R9  The paper leaves the gradient method open; the refinement here is
+ *       steepest descent with Armijo backtracking, integrals at off-grid
+ *       boundaries taken as the grid prefix plus the partial cell by the
+ *       same 8-point rule.
  *
  * Parity status: activations, fit, classify, pack/unpack and backward are
  * pinned by the CPU tests (closed forms, central differences, the paper's
@@ -358,6 +365,191 @@ int oracle_fit(int act, int bits, const oracle_weight* w_in, int64_t n,
 #undef DPX
 #undef BPX
     free(W); free(FW); free(F2); free(DP); free(BP);
+    return rc;
+}
+
+/* ------------------------------------------------------------------ */
+/* Gradient refinement of the boundaries (Sec. 3: y(s) of Eq. (4), the   */
+/* analytic gradient of L(s, y(s)) with respect to s, and the remark     */
+/* that the DP result may be finetuned by any gradient method).          */
+/* ------------------------------------------------------------------ */
+
+/* Integrals of w, f' w and f'^2 w over [A, x], A <= x <= B: the grid prefix
+ * up to the cell holding x plus the part of that cell below x, by the same
+ * 8-point rule (reading R3). */
+static void or_prefix_at(int act, const oracle_weight* w, int64_t n,
+                         const double* W, const double* FW, const double* F2,
+                         double x, double* pw, double* pfw, double* pf2w)
+{
+    double A = w->A, B = w->B;
+    int64_t j = (int64_t)floor((x - A) / (B - A) * (double)n);
+    if (j < 0) j = 0;
+    if (j > n) j = n;
+    double tj = A + (double)j * (B - A) / (double)n;
+    if (tj > x && j > 0) {          /* rounding put x just below t_j */
+        j -= 1;
+        tj = A + (double)j * (B - A) / (double)n;
+    }
+    double iw = 0.0, ifw = 0.0, if2w = 0.0;
+    if (j < n && x > tj) or_cell(act, w, tj, x, &iw, &ifw, &if2w);
+    *pw = W[j] + iw;
+    *pfw = FW[j] + ifw;
+    *pf2w = F2[j] + if2w;
+}
+
+/* L(s, y(s)) of Eq. (3) for interior boundaries s[0..K-2] (s_0 = A and
+ * s_K = B bound the outer intervals, reading R6), the values y(s) of
+ * Eq. (4) and, if grad != NULL, the gradient of Sec. 3:
+ *   dL/ds_i = (2 f'(s_i) - y_i - y_{i-1}) (y_i - y_{i-1}) w(s_i),
+ * y_{i-1} the value left of s_i and y_i the value right of it.
+ * Intervals without weight take f' at their midpoint and cost 0 (R4). */
+static double or_loss_at(int act, const oracle_weight* w, int64_t n,
+                         const double* W, const double* FW, const double* F2,
+                         int K, const double* s, double* y, double* grad)
+{
+    double edge[17];
+    edge[0] = w->A;
+    for (int m = 1; m < K; ++m) edge[m] = s[m - 1];
+    edge[K] = w->B;
+    double pw[17], pfw[17], pf2w[17];
+    for (int m = 0; m <= K; ++m)
+        or_prefix_at(act, w, n, W, FW, F2, edge[m], &pw[m], &pfw[m], &pf2w[m]);
+    double L = 0.0;
+    for (int m = 0; m < K; ++m) {
+        double dW = pw[m + 1] - pw[m];
+        double dFW = pfw[m + 1] - pfw[m];
+        double dF2 = pf2w[m + 1] - pf2w[m];
+        if (!(dW > 0.0)) {
+            y[m] = oracle_df(act, 0.5 * (edge[m] + edge[m + 1]));
+            continue;
+        }
+        y[m] = dFW / dW;
+        double T = dF2 - y[m] * y[m] * dW;
+        L += T > 0.0 ? T : 0.0;
+    }
+    if (grad)
+        for (int i = 1; i < K; ++i) {
+            double d = oracle_df(act, s[i - 1]);
+            grad[i - 1] = (2.0 * d - y[i] - y[i - 1]) * (y[i] - y[i - 1]) * or_w(w, s[i - 1]);
+        }
+    return L;
+}
+
+/* Exposed for the finite-difference test: L(s) (doubled for the symmetric
+ * fit), y(s) and dL/ds at the given boundaries. */
+int oracle_loss_at(int act, int bits, const oracle_weight* w_in, int64_t n,
+                   int symmetric, const double* s, double* y_out,
+                   double* grad_out, double* loss_out)
+{
+    if (bits < 1 || bits > 4 || n < 2) return -1;
+    const int K = 1 << bits;
+    oracle_weight w = *w_in;
+    if (symmetric && w.A < 0.0) w.A = 0.0;
+    double* W = (double*)malloc(sizeof(double) * (size_t)(n + 1));
+    double* FW = (double*)malloc(sizeof(double) * (size_t)(n + 1));
+    double* F2 = (double*)malloc(sizeof(double) * (size_t)(n + 1));
+    if (!W || !FW || !F2) { free(W); free(FW); free(F2); return -1; }
+    oracle_prefix(act, &w, n, W, FW, F2);
+    double scale = symmetric ? 2.0 : 1.0;
+    double L = or_loss_at(act, &w, n, W, FW, F2, K, s, y_out, grad_out);
+    if (grad_out)
+        for (int i = 0; i < K - 1; ++i) grad_out[i] *= scale;
+    *loss_out = scale * L;
+    free(W); free(FW); free(F2);
+    return 0;
+}
+
+/*
+ * The DP fit of oracle_fit, then gradient descent on the boundaries with
+ * the analytic gradient: from the DP cut points, step s <- s - t g, with t
+ * halved until the step keeps the boundaries strictly increasing inside
+ * (A, B) and decreases L, by at least 1e-4 t |g|^2 (Armijo), and doubled
+ * after each accepted step; the first step moves no boundary by more than
+ * one grid cell.  Stops after max_iter steps, or when no step decreases L.
+ *
+ *   s_out[K-1], v_out[K]  refined boundaries and values (fp32)
+ *   sd_out[K-1]           refined boundaries in double (may be NULL)
+ *   vd_out[K]             refined values in double (may be NULL)
+ *   loss_out              L after refinement (doubled for symmetric)
+ *   loss_dp_out           L of the DP result, same scale (may be NULL)
+ *   iters_out             accepted steps (may be NULL)
+ * Returns 0, -1 for bad arguments / allocation failure, -2 when the fp32
+ * boundaries are not strictly increasing.
+ */
+int oracle_fit_refined(int act, int bits, const oracle_weight* w_in, int64_t n,
+                       int symmetric, int max_iter, float* s_out, float* v_out,
+                       double* sd_out, double* vd_out, double* loss_out,
+                       double* loss_dp_out, int* iters_out)
+{
+    if (bits < 1 || bits > 4 || n < 2 || max_iter < 0) return -1;
+    const int K = 1 << bits;
+    int64_t cuts[17];
+    float s_dp[15], v_dp[16];
+    double loss_dp;
+    int rc = oracle_fit(act, bits, w_in, n, symmetric, s_dp, v_dp, &loss_dp, cuts,
+                        NULL, NULL);
+    if (rc == -1) return -1;
+
+    oracle_weight w = *w_in;
+    if (symmetric && w.A < 0.0) w.A = 0.0;
+    const double A = w.A, B = w.B, h = (B - A) / (double)n;
+    double* W = (double*)malloc(sizeof(double) * (size_t)(n + 1));
+    double* FW = (double*)malloc(sizeof(double) * (size_t)(n + 1));
+    double* F2 = (double*)malloc(sizeof(double) * (size_t)(n + 1));
+    if (!W || !FW || !F2) { free(W); free(FW); free(F2); return -1; }
+    oracle_prefix(act, &w, n, W, FW, F2);
+
+    double s[15], trial[15], g[15], y[16];
+    for (int m = 1; m < K; ++m) s[m - 1] = A + (double)cuts[m] * (B - A) / (double)n;
+    double L = or_loss_at(act, &w, n, W, FW, F2, K, s, y, g);
+    double gmax = 0.0;
+    for (int i = 0; i < K - 1; ++i) gmax = fmax(gmax, fabs(g[i]));
+    double t0 = gmax > 0.0 ? h / gmax : 0.0;
+    int it = 0;
+    while (it < max_iter && gmax > 0.0) {
+        double g2 = 0.0;
+        for (int i = 0; i < K - 1; ++i) g2 += g[i] * g[i];
+        double t = t0;
+        int accepted = 0;
+        for (int tries = 0; tries < 80; ++tries) {
+            int ok = 1;
+            for (int i = 0; i < K - 1; ++i) {
+                trial[i] = s[i] - t * g[i];
+                if (!(trial[i] > A && trial[i] < B)) ok = 0;
+                if (i > 0 && !(trial[i] > trial[i - 1])) ok = 0;
+            }
+            if (ok) {
+                double y_try[16];
+                double L_try = or_loss_at(act, &w, n, W, FW, F2, K, trial, y_try, NULL);
+                if (L_try < L && L_try <= L - 1e-4 * t * g2) { accepted = 1; break; }
+            }
+            t *= 0.5;
+        }
+        if (!accepted) break;
+        for (int i = 0; i < K - 1; ++i) s[i] = trial[i];
+        L = or_loss_at(act, &w, n, W, FW, F2, K, s, y, g);
+        gmax = 0.0;
+        for (int i = 0; i < K - 1; ++i) gmax = fmax(gmax, fabs(g[i]));
+        t0 = 2.0 * t;
+        ++it;
+    }
+
+    double scale = symmetric ? 2.0 : 1.0;
+    *loss_out = scale * L;
+    if (loss_dp_out) *loss_dp_out = loss_dp;
+    if (iters_out) *iters_out = it;
+    rc = 0;
+    for (int m = 0; m < K; ++m) {
+        v_out[m] = (float)y[m];
+        if (vd_out) vd_out[m] = y[m];
+    }
+    for (int m = 0; m < K - 1; ++m) {
+        s_out[m] = (float)s[m];
+        if (sd_out) sd_out[m] = s[m];
+    }
+    for (int m = 1; m + 1 < K; ++m)
+        if (!(s_out[m - 1] < s_out[m])) rc = -2;
+    free(W); free(FW); free(F2);
     return rc;
 }
 
