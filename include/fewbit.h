@@ -75,6 +75,9 @@ extern "C" {
 /* Table flags. */
 #define FEWBIT_FLAG_SYMMETRIC 1 /* even f': bins apply to |x|, fit on [0,B]
                                    (Fig. 3 caption)                        */
+/* Fit flag (fewbit_fit_table only; never set in a table). */
+#define FEWBIT_FLAG_REFINE    2 /* refine the DP boundaries by gradient
+                                   descent on L(s, y(s)) (Sec. 3)          */
 
 typedef struct fewbit_weight {
     int32_t kind;          /* FEWBIT_W_*                                   */
@@ -114,10 +117,17 @@ typedef struct fewbit_table {
  * by 8-point Gauss-Legendre quadrature per cell; every interval spans at
  * least one cell.  Values follow Eq. (4).  With FEWBIT_FLAG_SYMMETRIC the
  * fit is made on [max(A,0), B] for |x| and the reported loss is doubled.
+ * With FEWBIT_FLAG_REFINE the DP boundaries are then moved off the grid by
+ * steepest descent on L(s, y(s)) with its analytic gradient (Sec. 3),
+ * backtracking so that every step lowers L and keeps the boundaries sorted
+ * inside (A, B); integrals at off-grid points are the grid prefix plus the
+ * partial cell by the same rule.  The output table's flags keep only
+ * FEWBIT_FLAG_SYMMETRIC.
  * Runs on the host only; O(n_grid^2 * 2^bits) time, O(n_grid * 2^bits)
  * memory.  Deterministic.
  *
- *   act, bits, flags   as in fewbit_table (bits 1..4)
+ *   act, bits          as in fewbit_table (bits 1..4)
+ *   flags              FEWBIT_FLAG_SYMMETRIC and / or FEWBIT_FLAG_REFINE
  *   w                  weight function and support (host pointer)
  *   n_grid             number of grid cells, 2^bits <= n_grid <= 2^20
  *   out                receives the table (host pointer)

@@ -22,6 +22,7 @@ GELU, SILU, SIGMOID, TANH, RELU, SELU, SOFTPLUS = 0, 1, 2, 3, 4, 5, 6
 F32, F16, BF16 = 0, 1, 2
 W_UNIFORM, W_NORMAL, W_MIXTURE = 0, 1, 2
 FLAG_SYMMETRIC = 1
+FLAG_REFINE = 2
 
 ACTS = {"gelu": GELU, "silu": SILU, "swish": SILU, "sigmoid": SIGMOID, "tanh": TANH,
         "relu": RELU, "selu": SELU, "softplus": SOFTPLUS}
@@ -146,13 +147,15 @@ class Table:
         return Table(ct)
 
 
-def fit_table(act, bits: int, weight: Weight, n_grid: int, symmetric: bool = False) -> Table:
-    """fewbit_fit_table: the dynamic-programming fit of Sec. 3 (host)."""
+def fit_table(act, bits: int, weight: Weight, n_grid: int, symmetric: bool = False,
+              refine: bool = False) -> Table:
+    """fewbit_fit_table: the dynamic-programming fit of Sec. 3 (host), with
+    refine=True followed by gradient descent on the boundaries."""
     a = ACTS[act] if isinstance(act, str) else int(act)
     ct = CTable()
     cw = weight.c()
-    rc = lib.fewbit_fit_table(a, int(bits), C.byref(cw), int(n_grid),
-                              FLAG_SYMMETRIC if symmetric else 0, C.byref(ct))
+    flags = (FLAG_SYMMETRIC if symmetric else 0) | (FLAG_REFINE if refine else 0)
+    rc = lib.fewbit_fit_table(a, int(bits), C.byref(cw), int(n_grid), flags, C.byref(ct))
     if rc != OK:
         raise FewbitError(rc, "fewbit_fit_table")
     return Table(ct)

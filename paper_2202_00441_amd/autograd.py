@@ -27,17 +27,18 @@ class FewBitAct(torch.nn.Module):
     """Few-bit GELU / SiLU / Sigmoid / Tanh / ReLU / SELU / Softplus.
 
     The table is fitted once at construction (Sec. 3); by default under a
-    standard normal weight on [-10, 10] with a 4000-cell grid.
+    standard normal weight on [-10, 10] with a 4000-cell grid, optionally
+    refined by gradient descent on the boundaries.
     """
 
     def __init__(self, act: str = "gelu", bits: int = 3, weight: Weight | None = None,
-                 n_grid: int = 4000, table: Table | None = None):
+                 n_grid: int = 4000, table: Table | None = None, refine: bool = False):
         super().__init__()
         self.act = act
         self.bits = bits
         if table is None:
             weight = weight or Weight(W_NORMAL, -10.0, 10.0)
-            table = fit_table(ACTS[act], bits, weight, n_grid)
+            table = fit_table(ACTS[act], bits, weight, n_grid, refine=refine)
         self.table = table
 
     def forward(self, x):

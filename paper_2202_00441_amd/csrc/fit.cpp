@@ -15,7 +15,10 @@
 //     computed here by Newton's method on the Legendre polynomial;
 //   * an interval with no weight costs 0 and takes f' at its midpoint; a
 //     negative cost from cancellation is clamped to 0;
-//   * every interval spans at least one cell; ties keep the leftmost cut.
+//   * every interval spans at least one cell; ties keep the leftmost cut;
+//   * FEWBIT_FLAG_REFINE: the DP result is then refined by steepest descent
+//     with the analytic gradient of Sec. 3 and backtracking, integrals at
+//     off-grid boundaries taken as grid prefix plus partial cell.
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -122,6 +125,10 @@ Rule legendre_rule8() {
 
 bool is_finite_value(double v) { return std::isfinite(v); }
 
+// Upper bound on accepted descent steps of the refinement (it stops earlier
+// once no step lowers L).
+constexpr int kRefineMaxSteps = 20000;
+
 }  // namespace
 
 extern "C" int fewbit_fit_table(int32_t act, int32_t bits, const fewbit_weight* w,
@@ -129,7 +136,7 @@ extern "C" int fewbit_fit_table(int32_t act, int32_t bits, const fewbit_weight* 
   if (!w || !out) return FEWBIT_E_NULL;
   if (bits < 1 || bits > 4) return FEWBIT_E_BITS;
   if (act < FEWBIT_GELU || act > FEWBIT_SOFTPLUS) return FEWBIT_E_INVALID;
-  if (flags & ~FEWBIT_FLAG_SYMMETRIC) return FEWBIT_E_INVALID;
+  if (flags & ~(FEWBIT_FLAG_SYMMETRIC | FEWBIT_FLAG_REFINE)) return FEWBIT_E_INVALID;
   if (w->reserved != 0) return FEWBIT_E_INVALID;
   if (w->kind < FEWBIT_W_UNIFORM || w->kind > FEWBIT_W_MIXTURE) return FEWBIT_E_INVALID;
   if (!is_finite_value(w->A) || !is_finite_value(w->B) || !(w->A < w->B)) return FEWBIT_E_INVALID;
@@ -163,12 +170,11 @@ extern "C" int fewbit_fit_table(int32_t act, int32_t bits, const fewbit_weight* 
     return FEWBIT_E_NOMEM;
   }
 
-  // prefix integrals of w, f' w, f'^2 w over the cells (Eqs. (8)-(9))
+  // integrals of w, f' w, f'^2 w over [a, b] by the 8-point rule
   const Rule rule = legendre_rule8();
-  for (int64_t i = 0; i < n; ++i) {
-    const double a = grid(i), b = grid(i + 1);
+  auto quad = [&](double a, double b, double& s0, double& s1, double& s2) {
     const double mid = 0.5 * (a + b), half = 0.5 * (b - a);
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0;
+    s0 = s1 = s2 = 0.0;
     for (int k = 0; k < 8; ++k) {
       const double x = mid + half * rule.node[k];
       const double wx = wt(x);
@@ -177,9 +183,17 @@ extern "C" int fewbit_fit_table(int32_t act, int32_t bits, const fewbit_weight* 
       s1 += rule.weight[k] * d * wx;
       s2 += rule.weight[k] * d * d * wx;
     }
-    W[i + 1] = W[i] + half * s0;
-    FW[i + 1] = FW[i] + half * s1;
-    F2[i + 1] = F2[i] + half * s2;
+    s0 *= half;
+    s1 *= half;
+    s2 *= half;
+  };
+  // prefix integrals over the cells (Eqs. (8)-(9))
+  for (int64_t i = 0; i < n; ++i) {
+    double c0, c1, c2;
+    quad(grid(i), grid(i + 1), c0, c1, c2);
+    W[i + 1] = W[i] + c0;
+    FW[i + 1] = FW[i] + c1;
+    F2[i + 1] = F2[i] + c2;
   }
 
   // cost of one interval [t_j, t_i]: F2 diff minus y^2 times W diff (Eq. (8))
@@ -233,15 +247,103 @@ extern "C" int fewbit_fit_table(int32_t act, int32_t bits, const fewbit_weight* 
     cut[k - 1] = back[static_cast<size_t>(k) * (n + 1) + static_cast<size_t>(cut[k])];
   cut[0] = 0;
 
+  // boundaries and values of the DP result
+  double bnd[17], val[16];
+  bnd[0] = lo;
+  bnd[K] = hi;
+  for (int m = 1; m < K; ++m) bnd[m] = grid(cut[m]);
+  for (int m = 0; m < K; ++m) val[m] = interval_value(cut[m], cut[m + 1]);
+  double loss = cost_prev[n];
+
+  if (flags & FEWBIT_FLAG_REFINE) {
+    // L(s, y(s)) at off-grid boundaries: each integral over [lo, x] is the
+    // grid prefix up to the cell holding x plus the part of that cell below
+    // x, by the same rule.  Values by Eq. (4); gradient of Sec. 3,
+    //   dL/ds_m = (2 f'(s_m) - y_m - y_{m-1}) (y_m - y_{m-1}) w(s_m).
+    auto upto = [&](double x, double& p0, double& p1, double& p2) {
+      int64_t j = static_cast<int64_t>(std::floor((x - lo) / (hi - lo) * static_cast<double>(n)));
+      j = j < 0 ? 0 : (j > n ? n : j);
+      if (j > 0 && grid(j) > x) --j;
+      p0 = W[j];
+      p1 = FW[j];
+      p2 = F2[j];
+      if (j < n && x > grid(j)) {
+        double c0, c1, c2;
+        quad(grid(j), x, c0, c1, c2);
+        p0 += c0;
+        p1 += c1;
+        p2 += c2;
+      }
+    };
+    auto evaluate = [&](const double* e, double* y, double* grad) {
+      double P0[17], P1[17], P2[17];
+      for (int m = 0; m <= K; ++m) upto(e[m], P0[m], P1[m], P2[m]);
+      double L = 0.0;
+      for (int m = 0; m < K; ++m) {
+        const double dw = P0[m + 1] - P0[m];
+        if (!(dw > 0.0)) {
+          y[m] = activation_derivative(act, 0.5 * (e[m] + e[m + 1]));
+          continue;
+        }
+        y[m] = (P1[m + 1] - P1[m]) / dw;
+        const double c = (P2[m + 1] - P2[m]) - y[m] * y[m] * dw;
+        L += c > 0.0 ? c : 0.0;
+      }
+      if (grad)
+        for (int m = 1; m < K; ++m)
+          grad[m] = (2.0 * activation_derivative(act, e[m]) - y[m] - y[m - 1]) *
+                    (y[m] - y[m - 1]) * wt(e[m]);
+      return L;
+    };
+    // steepest descent with backtracking: a step must keep the boundaries
+    // strictly increasing inside (lo, hi) and lower L by 1e-4 t |g|^2; the
+    // first step moves a boundary by at most one cell, and each accepted
+    // step doubles the next trial step
+    double g[17], y[16], trial[17], ytrial[16];
+    double L = evaluate(bnd, y, g);
+    auto max_abs = [&](const double* v) {
+      double r = 0.0;
+      for (int m = 1; m < K; ++m) r = std::fmax(r, std::fabs(v[m]));
+      return r;
+    };
+    double step = max_abs(g) > 0.0 ? (hi - lo) / static_cast<double>(n) / max_abs(g) : 0.0;
+    for (int iter = 0; iter < kRefineMaxSteps && max_abs(g) > 0.0; ++iter) {
+      double g2 = 0.0;
+      for (int m = 1; m < K; ++m) g2 += g[m] * g[m];
+      bool accepted = false;
+      for (int halvings = 0; halvings < 80 && !accepted; ++halvings) {
+        bool sorted = true;
+        trial[0] = lo;
+        trial[K] = hi;
+        for (int m = 1; m < K; ++m) {
+          trial[m] = bnd[m] - step * g[m];
+          sorted = sorted && trial[m] > trial[m - 1];
+        }
+        sorted = sorted && trial[K - 1] < hi;
+        if (sorted) {
+          const double Lt = evaluate(trial, ytrial, nullptr);
+          accepted = Lt < L && Lt <= L - 1e-4 * step * g2;
+        }
+        if (!accepted) step *= 0.5;
+      }
+      if (!accepted) break;
+      for (int m = 1; m < K; ++m) bnd[m] = trial[m];
+      L = evaluate(bnd, y, g);
+      step *= 2.0;
+    }
+    for (int m = 0; m < K; ++m) val[m] = y[m];
+    loss = L;
+  }
+
   fewbit_table t;
   std::memset(&t, 0, sizeof t);
   t.act = act;
   t.bits = bits;
-  t.flags = flags;
+  t.flags = flags & FEWBIT_FLAG_SYMMETRIC;
   for (int m = 0; m < 15; ++m) t.s[m] = INFINITY;
-  for (int m = 1; m < K; ++m) t.s[m - 1] = static_cast<float>(grid(cut[m]));
-  for (int m = 0; m < K; ++m) t.v[m] = static_cast<float>(interval_value(cut[m], cut[m + 1]));
-  t.loss = (sym ? 2.0 : 1.0) * cost_prev[n];
+  for (int m = 1; m < K; ++m) t.s[m - 1] = static_cast<float>(bnd[m]);
+  for (int m = 0; m < K; ++m) t.v[m] = static_cast<float>(val[m]);
+  t.loss = (sym ? 2.0 : 1.0) * loss;
   for (int m = 1; m + 1 < K; ++m)
     if (!(t.s[m - 1] < t.s[m])) return FEWBIT_E_NUMERIC;
   for (int m = 0; m < K; ++m)
