@@ -206,6 +206,9 @@ def main():
     ap.add_argument("--bits", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--memory", action="store_true",
+                    help="report activation memory held for backward, vanilla vs few-bit, on a "
+                         "GPT-2-small-shaped stack of feed-forward blocks, instead of timing")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="summarise a rocprofv3 --kernel-trace --stats output directory")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -230,6 +233,22 @@ def main():
     import torch
     import workloads as WL
     import paper_2202_00441_amd as P
+
+    if args.memory:
+        from paper_2202_00441_amd.memory import compare
+        torch.cuda.set_device(0)
+        rows = []
+        for dtype in (torch.bfloat16, torch.float32):
+            for bits in (1, 2, 3, 4):
+                rows.append(compare(d=768, d_ff=3072, layers=12, tokens=8 * 256, bits=bits,
+                                    dtype=dtype))
+        print(json.dumps({
+            "metric": "activation memory held for backward, vanilla vs few-bit GELU",
+            "config": {"workload": "12 feed-forward blocks x -> x + W2 GELU(W1 x), d 768, "
+                                   "d_ff 3072 (GPT-2 small), 8 x 256 tokens, random weights"},
+            "rows": rows,
+        }), flush=True)
+        return
 
     w = WL.WORKLOADS[args.workload]
     bits = args.bits
