@@ -54,6 +54,11 @@
 #ifndef FEWBIT_FWD16_UNROLL
 #define FEWBIT_FWD16_UNROLL 4
 #endif
+// waves per fp16 / bf16 forward workgroup that stream after the tables are
+// built (all of them build the tables; the rest then exit)
+#ifndef FEWBIT_FWD16_STREAM_WAVES
+#define FEWBIT_FWD16_STREAM_WAVES (FEWBIT_FWD16_THREADS / 64)
+#endif
 #ifndef FEWBIT_FWD32_THREADS
 #define FEWBIT_FWD32_THREADS 256
 #endif
@@ -67,10 +72,10 @@
 #define FEWBIT_BWD_THREADS 512
 #endif
 #ifndef FEWBIT_BWD_WG_PER_CU
-#define FEWBIT_BWD_WG_PER_CU 2
+#define FEWBIT_BWD_WG_PER_CU 1
 #endif
 #ifndef FEWBIT_BWD_UNROLL
-#define FEWBIT_BWD_UNROLL 2
+#define FEWBIT_BWD_UNROLL 4
 #endif
 #ifndef FEWBIT_NT_LOADS
 #define FEWBIT_NT_LOADS 1             // non-temporal stream loads
@@ -177,14 +182,11 @@ struct Scalar<FEWBIT_F32> {
 // the smallest shift that keeps every product representable in the output
 // type (fp16 outputs underflow long before 2^-126, so S = 0 there).
 //
-// |x| * tail uses the multiply in which 0 * x = 0 for every x, so x = +-inf
-// (where the tail is 0) gives relu(x) exactly without a separate clamp.  The
-// absolute value is a source modifier of the instruction.
-__device__ inline float abs_mul_zero_wins(float x, float b) {
-  float r;
-  asm("v_mul_legacy_f32_e64 %0, |%1|, %2" : "=v"(r) : "v"(x), "v"(b));
-  return r;
-}
+// In the product |x| * tail, |x| is clamped to the largest finite float:
+// for x = +-inf the other factor is exactly 0 and the product is 0 (not
+// inf * 0), so f(x) = relu(x) without a separate branch; NaN still reaches
+// the result through the exponential's argument, which is not clamped.
+__device__ inline float finite_abs(float x) { return fminf(fabsf(x), 3.4028234663852886e38f); }
 
 // max(x, -0) as one integer op: the unsigned minimum with the bits of -0
 // keeps every float with the sign bit clear (+inf, NaN included) and maps
@@ -260,14 +262,14 @@ struct Act<DT, FEWBIT_GELU> {
                   : static_cast<float>(static_cast<double>(F::c[i]) * pow2(S * i));
   }
   __device__ static float f(float x) {
-    const float t = fabsf(x);
+    const float t = finite_abs(x);
     const float rs = __builtin_amdgcn_rcpf(
         fmaf(t, static_cast<float>(F::p * pow2(S)), static_cast<float>(pow2(S))));  // 2^-S r
     float c = coef(D);
 #pragma unroll
     for (int i = D - 1; i >= 0; --i) c = fmaf(c, rs, coef(i));
     const float e = __builtin_amdgcn_exp2f(fmaf(x * x, -kHalfLog2e, c));    // 2^S Q(t) / r
-    return fmaf(-abs_mul_zero_wins(x, rs), e, relu(x));   // relu(x) - t Q(t); NaN via x*x
+    return fmaf(-(t * rs), e, relu(x));   // relu(x) - t Q(t); NaN via x*x
   }
 };
 
@@ -275,10 +277,9 @@ template <int DT>
 struct Act<DT, FEWBIT_SILU> {
   static constexpr int S = Prec<DT>::kSiluS;
   __device__ static float f(float x) {
-    const float t = fabsf(x);
-    const float e = __builtin_amdgcn_exp2f(fmaf(t, -kLog2e, static_cast<float>(S)));  // 2^S e^-t
+    const float e = __builtin_amdgcn_exp2f(fmaf(fabsf(x), -kLog2e, static_cast<float>(S)));  // 2^S e^-t
     const float r = __builtin_amdgcn_rcpf(e + static_cast<float>(pow2(S)));  // 1/(2^S (1 + e^-t))
-    return fmaf(-abs_mul_zero_wins(x, e), r, relu(x));    // relu(x) - t sigma(-t)
+    return fmaf(-(finite_abs(x) * e), r, relu(x));    // relu(x) - t sigma(-t); NaN via e
   }
 };
 
@@ -402,16 +403,56 @@ __device__ inline uint32_t load_field(const uint32_t* base, int lane, int64_t va
   }
 }
 
+// The same two layouts for a full tile, with every lane active: in the
+// loops over full tiles no lane is masked off, so no branch splits the loop
+// body and the compiler can keep all of a group's loads in flight.  When
+// packing, a lane without a word of its own stores an identical copy of a
+// neighbour's word to the same address; when unpacking, lane 3 of each quad
+// reloads word 2 of the quad, which the permutes never read.
+template <int BITS>
+__device__ inline void pack_store_full(uint32_t* out, uint32_t F, int lane) {
+  if constexpr (BITS == 4) {
+    st_word(out + lane, F);
+  } else if constexpr (BITS == 2) {
+    const uint32_t lo = quad_read<quad_perm(0, 0, 2, 2)>(F);
+    const uint32_t hi = quad_read<quad_perm(1, 1, 3, 3)>(F);
+    st_word(out + (lane >> 1), lo | (hi << 16));
+  } else if constexpr (BITS == 1) {
+    const uint32_t a = quad_read<quad_perm(0, 0, 2, 2)>(F) | (quad_read<quad_perm(1, 1, 3, 3)>(F) << 8);
+    const uint32_t w = quad_read<quad_perm(0, 0, 0, 0)>(a) | (quad_read<quad_perm(2, 2, 2, 2)>(a) << 16);
+    st_word(out + (lane >> 2), w);
+  } else {  // BITS == 3: lane k of a quad writes word min(k, 2) of the quad
+    const int j = min(lane & 3, 2);
+    const uint32_t lo = quad_read<quad_perm(0, 1, 2, 2)>(F);
+    const uint32_t hi = quad_read<quad_perm(1, 2, 3, 3)>(F);
+    st_word(out + 3 * (lane >> 2) + j, (lo >> (8 * j)) | (hi << (24 - 8 * j)));
+  }
+}
+
+template <int BITS>
+__device__ inline uint32_t load_field_full(const uint32_t* base, int lane) {
+  if constexpr (BITS == 3) {
+    const int k = lane & 3;
+    const uint32_t w = ld_word(base + 3 * (lane >> 2) + min(k, 2));
+    const uint32_t prev = quad_read<quad_perm(0, 0, 1, 2)>(w);   // word k-1 (k = 0: word 0)
+    const uint32_t own = quad_read<quad_perm(0, 1, 2, 2)>(w);    // word k (k = 3: word 2)
+    return __builtin_amdgcn_alignbit(own, prev, (24 * k) & 31);
+  } else {
+    return ld_word(base + ((8 * BITS * lane) >> 5)) >> ((8 * BITS * lane) & 31);
+  }
+}
+
 struct WaveIndex {
   int lane;
   int64_t wave, nwaves;
 };
-__device__ inline WaveIndex wave_index() {
-  const int per_block = blockDim.x / kWave;
+// Waves 0 .. per_block-1 of every workgroup, numbered across the grid.
+__device__ inline WaveIndex wave_index_of(int per_block) {
   return {static_cast<int>(threadIdx.x & (kWave - 1)),
           static_cast<int64_t>(blockIdx.x) * per_block + (threadIdx.x / kWave),
           static_cast<int64_t>(gridDim.x) * per_block};
 }
+__device__ inline WaveIndex wave_index() { return wave_index_of(blockDim.x / kWave); }
 
 // ---------------------------------------------------------------- forward, fp16 / bf16
 // For 16-bit inputs both results of the forward are functions of the input
@@ -543,7 +584,10 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   __builtin_amdgcn_s_waitcnt(0);     // the table loads have landed in LDS
   __syncthreads();
 
-  const WaveIndex wi = wave_index();
+  constexpr int kStream = FEWBIT_FWD16_STREAM_WAVES;
+  static_assert(kStream >= 1 && kStream <= FEWBIT_FWD16_THREADS / kWave, "stream waves");
+  if (static_cast<int>(threadIdx.x / kWave) >= kStream) return;   // no barrier follows
+  const WaveIndex wi = wave_index_of(kStream);
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
@@ -559,7 +603,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
-      pack_store<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane, kWords);
+      pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
     }
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
@@ -567,7 +611,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
     uint32_t F;
     fwd16_tile<BITS>(ld_stream(x + t * kTile + lane_off), ylut, clut, out, F);
     st_stream(y + t * kTile + lane_off, out);
-    pack_store<BITS>(codes + t * kWords, F, wi.lane, kWords);
+    pack_store_full<BITS>(codes + t * kWords, F, wi.lane);
   }
   // the partial tile at the end, if any, goes to the wave that would own it
   if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
@@ -628,7 +672,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
       float* q = y + (t0 + u) * kTile + lane_off;
       st_stream(q, out[u][0]);
       st_stream(q + 4, out[u][1]);
-      pack_store<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane, kWords);
+      pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
     }
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
@@ -639,7 +683,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
     fwd32_tile<BITS, ACT>(in, tab, symmetric, out, F);
     st_stream(y + t * kTile + lane_off, out[0]);
     st_stream(y + t * kTile + lane_off + 4, out[1]);
-    pack_store<BITS>(codes + t * kWords, F, wi.lane, kWords);
+    pack_store_full<BITS>(codes + t * kWords, F, wi.lane);
   }
   if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
     const int64_t t = full;
@@ -729,7 +773,7 @@ __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
       const char* p = gb + ((t0 + u) * kTile + lane_off) * kEsz;
 #pragma unroll
       for (int v = 0; v < V; ++v) in[u][v] = ld_stream(p + 16 * v);
-      F[u] = load_field<BITS>(codes + (t0 + u) * kWords, wi.lane, kWords);
+      F[u] = load_field_full<BITS>(codes + (t0 + u) * kWords, wi.lane);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) Grad<DT, BITS>::apply(in[u], F[u], pairs, out[u]);
@@ -745,7 +789,7 @@ __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
     const char* p = gb + (t * kTile + lane_off) * kEsz;
 #pragma unroll
     for (int v = 0; v < V; ++v) in[v] = ld_stream(p + 16 * v);
-    const uint32_t F = load_field<BITS>(codes + t * kWords, wi.lane, kWords);
+    const uint32_t F = load_field_full<BITS>(codes + t * kWords, wi.lane);
     Grad<DT, BITS>::apply(in, F, pairs, out);
     char* q = ob + (t * kTile + lane_off) * kEsz;
 #pragma unroll
@@ -809,9 +853,10 @@ int device_cus() {
   return c;
 }
 
-dim3 grid_for(int64_t n, int threads, int wg_per_cu) {
+// Workgroups for n elements when each has `waves_per_block` streaming waves:
+// one tile per wave at most, capped at wg_per_cu per compute unit.
+dim3 grid_for(int64_t n, int waves_per_block, int wg_per_cu) {
   const int64_t tiles = (n + kTile - 1) / kTile;
-  const int waves_per_block = threads / kWave;
   int64_t blocks = (tiles + waves_per_block - 1) / waves_per_block;
   const int64_t cap = static_cast<int64_t>(device_cus()) * wg_per_cu;
   if (blocks > cap) blocks = cap;
@@ -864,13 +909,13 @@ void launch_fwd(const Launch& L) {
   const int64_t nw = (L.n * BITS + 31) / 32;
   const int sym = (L.t->flags & FEWBIT_FLAG_SYMMETRIC) ? 1 : 0;
   if constexpr (DT == FEWBIT_F32) {
-    const dim3 grid = grid_for(L.n, FEWBIT_FWD32_THREADS, FEWBIT_FWD32_WG_PER_CU);
+    const dim3 grid = grid_for(L.n, FEWBIT_FWD32_THREADS / kWave, FEWBIT_FWD32_WG_PER_CU);
     (void)hipGetLastError();
     hipLaunchKernelGGL((fwd32_kernel<BITS, ACT>), grid, dim3(FEWBIT_FWD32_THREADS), 0, L.s,
                        static_cast<const float*>(L.in), static_cast<float*>(L.out), L.codes, L.n,
                        nw, table_args(L.t), sym);
   } else {
-    const dim3 grid = grid_for(L.n, FEWBIT_FWD16_THREADS, FEWBIT_FWD16_WG_PER_CU);
+    const dim3 grid = grid_for(L.n, FEWBIT_FWD16_STREAM_WAVES, FEWBIT_FWD16_WG_PER_CU);
     (void)hipGetLastError();
     hipLaunchKernelGGL((fwd16_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16_THREADS), 0, L.s,
                        static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
@@ -904,7 +949,7 @@ void launch_fwd_bits(const Launch& L) {
 template <int DT, int BITS>
 void launch_bwd(const Launch& L) {
   const int64_t nw = (L.n * BITS + 31) / 32;
-  const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS, FEWBIT_BWD_WG_PER_CU);
+  const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS / kWave, FEWBIT_BWD_WG_PER_CU);
   (void)hipGetLastError();
   hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s, L.in,
                      L.codes, L.out, L.n, nw, table_args(L.t));
