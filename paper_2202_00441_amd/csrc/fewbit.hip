@@ -54,6 +54,11 @@
 #ifndef FEWBIT_FWD16_UNROLL
 #define FEWBIT_FWD16_UNROLL 4
 #endif
+// 1: the fp16 / bf16 forward loads the next group of tiles before it looks
+// up the current one, so loads stay in flight during the LDS lookups
+#ifndef FEWBIT_FWD16_PIPELINE
+#define FEWBIT_FWD16_PIPELINE 0
+#endif
 // waves per fp16 / bf16 forward workgroup that stream after the tables are
 // built (all of them build the tables; the rest then exit)
 #ifndef FEWBIT_FWD16_STREAM_WAVES
@@ -124,9 +129,8 @@ struct Half<FEWBIT_BF16> {
   __device__ static uint32_t pack(float a, float b) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
   }
-  // runs of 16 patterns with the exponent all ones: infinity, then NaNs
-  __device__ static bool special_run(uint32_t p) { return (p & 0x7F80u) == 0x7F80u; }
-  static constexpr uint32_t kMantissa = 0x7Fu;
+  // magnitudes from here up: exponent all ones (infinity, NaNs)
+  static constexpr uint32_t kSpecialFrom = 0x7F80u;
 };
 
 template <>
@@ -148,8 +152,7 @@ struct Half<FEWBIT_F16> {
     asm("" : "+v"(a), "+v"(b));
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, f16x2_t));
   }
-  __device__ static bool special_run(uint32_t p) { return (p & 0x7C00u) == 0x7C00u; }
-  static constexpr uint32_t kMantissa = 0x3FFu;
+  static constexpr uint32_t kSpecialFrom = 0x7C00u;
 };
 
 // element-wise access for the partial tile at the end
@@ -470,11 +473,11 @@ __device__ inline WaveIndex wave_index() { return wave_index_of(blockDim.x / kWa
 // storage type) into a static device array, before the first fp16 / bf16
 // forward on that device; each workgroup copies the one it needs into LDS
 // with direct global-to-LDS loads.  clut depends on the boundaries and is
-// built by every workgroup: the index is monotone in the value within a run
-// of 16 patterns that share sign and exponent, so a run whose two ends agree
-// is filled without evaluating the rest, and the runs of infinities and
-// NaNs by rule (an infinity opens its run, every NaN takes index 0); only
-// runs holding a boundary are classified pattern by pattern.
+// built by every workgroup: the index is monotone in the pattern within one
+// sign, so each thread classifies only the two ends of its segment of
+// patterns and fills it if they agree; the few segments that hold a
+// boundary, infinities or NaNs are then classified pattern by pattern by
+// the whole wave.
 constexpr int kActs = FEWBIT_SOFTPLUS + 1;
 __device__ __attribute__((aligned(16))) uint16_t g_ytab[kActs][2][65536];
 
@@ -525,28 +528,37 @@ __device__ void load_output_table(uint16_t* ylut) {
 
 template <int DT, int BITS>
 __device__ void build_code_table(uint8_t* clut, const TableArgs& tab, int symmetric) {
+  // each thread owns one aligned segment of kSeg patterns (kSeg / 2 bytes)
+  constexpr uint32_t kSeg = 65536u / FEWBIT_FWD16_THREADS;
+  static_assert(kSeg >= 32 && kSeg <= 32768 && 65536u % FEWBIT_FWD16_THREADS == 0,
+                "segments of whole 16-byte stores within one sign");
   auto code_of = [&](uint32_t p) {
     const float v = Half<DT>::widen(p);
     return classify<BITS>(symmetric ? fabsf(v) : v, tab);
   };
-  for (uint32_t run = threadIdx.x; run < 4096u; run += FEWBIT_FWD16_THREADS) {
-    const uint32_t p0 = run * 16u;
-    const uint32_t a = code_of(p0), b = code_of(p0 + 15u);
-    uint32_t q0, q1;
-    if (Half<DT>::special_run(p0)) {
-      // an infinity opens the first such run (its index is a); NaNs take 0
-      q0 = ((p0 & Half<DT>::kMantissa) == 0u) ? a : 0u;
-      q1 = 0u;
-    } else if (a == b) {
-      q0 = q1 = a * 0x11111111u;
-    } else {
-      q0 = q1 = 0u;
-      for (uint32_t k = 0; k < 8u; ++k) {
-        q0 |= code_of(p0 + k) << (4u * k);
-        q1 |= code_of(p0 + 8u + k) << (4u * k);
-      }
-    }
-    *reinterpret_cast<uint2*>(clut + run * 8u) = make_uint2(q0, q1);
+  const uint32_t p0 = threadIdx.x * kSeg;
+  const uint32_t last = p0 + kSeg - 1u;
+  // the index is monotone in the pattern within one sign, so a segment
+  // whose two ends agree is uniform, unless it reaches the infinities and
+  // NaNs at the top of its sign (exponent all ones)
+  const bool special = (last & 0x7FFFu) >= Half<DT>::kSpecialFrom;
+  const uint32_t a = code_of(p0);
+  const bool uniform = !special && a == code_of(last);
+  if (uniform) {
+    const uint32_t rep = a * 0x11111111u;
+#pragma unroll
+    for (uint32_t i = 0; i < kSeg / 32u; ++i)
+      reinterpret_cast<u32x4_t*>(clut + p0 / 2u)[i] = (u32x4_t){rep, rep, rep, rep};
+  }
+  // the other segments are classified pattern by pattern by the whole wave
+  const uint32_t lane = threadIdx.x & (kWave - 1), first = threadIdx.x - lane;
+  uint64_t todo = __ballot(!uniform);
+  while (todo) {
+    const uint32_t l = static_cast<uint32_t>(__builtin_ctzll(todo));
+    todo &= todo - 1u;
+    const uint32_t q0 = (first + l) * kSeg;
+    for (uint32_t j = 2u * lane; j < kSeg; j += 2u * kWave)
+      clut[(q0 + j) / 2u] = static_cast<uint8_t>(code_of(q0 + j) | (code_of(q0 + j + 1u) << 4));
   }
 }
 
@@ -592,18 +604,44 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
 
-  for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
-    const int64_t t0 = gi * U;
-    u32x4_t in[U], out[U];
-    uint32_t F[U];
+  if constexpr (FEWBIT_FWD16_PIPELINE) {
+    u32x4_t in[U];
+    if (wi.wave < groups) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (t0 + u) * kTile + lane_off);
+      for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (wi.wave * U + u) * kTile + lane_off);
+    }
+    for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
+      const int64_t t0 = gi * U, next = gi + wi.nwaves;
+      u32x4_t nx[U], out[U];
+      uint32_t F[U];
+      if (next < groups) {      // the same for the whole wave
 #pragma unroll
-    for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
+        for (int u = 0; u < U; ++u) nx[u] = ld_stream(x + (next * U + u) * kTile + lane_off);
+      }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
-      pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
+      for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
+        pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) in[u] = nx[u];
+    }
+  } else {
+    for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
+      const int64_t t0 = gi * U;
+      u32x4_t in[U], out[U];
+      uint32_t F[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (t0 + u) * kTile + lane_off);
+#pragma unroll
+      for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
+        pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
+      }
     }
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
