@@ -65,13 +65,13 @@
 #define FEWBIT_FWD16_STREAM_WAVES (FEWBIT_FWD16_THREADS / 64)
 #endif
 #ifndef FEWBIT_FWD32_THREADS
-#define FEWBIT_FWD32_THREADS 256
+#define FEWBIT_FWD32_THREADS 512
 #endif
 #ifndef FEWBIT_FWD32_WG_PER_CU
-#define FEWBIT_FWD32_WG_PER_CU 4
+#define FEWBIT_FWD32_WG_PER_CU 2
 #endif
 #ifndef FEWBIT_FWD32_UNROLL
-#define FEWBIT_FWD32_UNROLL 2
+#define FEWBIT_FWD32_UNROLL 1
 #endif
 #ifndef FEWBIT_BWD_THREADS
 #define FEWBIT_BWD_THREADS 512
@@ -81,6 +81,9 @@
 #endif
 #ifndef FEWBIT_BWD_UNROLL
 #define FEWBIT_BWD_UNROLL 4
+#endif
+#ifndef FEWBIT_BWD32_UNROLL             // fp32 tiles are twice the bytes
+#define FEWBIT_BWD32_UNROLL 2
 #endif
 #ifndef FEWBIT_NT_LOADS
 #define FEWBIT_NT_LOADS 1             // non-temporal stream loads
@@ -198,11 +201,15 @@ __device__ inline float relu(float x) {
   return __uint_as_float(min(__float_as_uint(x), 0x80000000u));
 }
 
+// 2^e for -1022 <= e <= 1023, from the exponent field
 constexpr double pow2(int e) {
-  double r = 1.0;
-  for (int i = 0; i < (e < 0 ? -e : e); ++i) r = (e < 0) ? r * 0.5 : r * 2.0;
-  return r;
+  return __builtin_bit_cast(double, static_cast<uint64_t>(1023 + e) << 52);
 }
+
+template <int N>
+struct Coefs {
+  float c[N];
+};
 
 // GELU: the normal upper tail Q(t) = P(Z > t) = r exp2(c(r) - t^2/(2 ln 2))
 // with r = 1/(1 + p t) and c a polynomial in r (the form of the Chebyshev
@@ -259,18 +266,23 @@ template <int DT>
 struct Act<DT, FEWBIT_GELU> {
   static constexpr int D = Prec<DT>::kGeluDeg, S = Prec<DT>::kGeluS;
   using F = QFit<D>;
-  // coefficients of c in r' = 2^-S r: c_i 2^(S i), and c_0 + S
-  static constexpr float coef(int i) {
-    return i == 0 ? F::c[0] + static_cast<float>(S)
-                  : static_cast<float>(static_cast<double>(F::c[i]) * pow2(S * i));
-  }
+  // coefficients of c in r' = 2^-S r: c_i 2^(S i), and c_0 + S (evaluated
+  // at compile time: constant-initialised)
+  static constexpr Coefs<D + 1> kCoef = [] {
+    Coefs<D + 1> a{};
+    for (int i = 0; i <= D; ++i)
+      a.c[i] = i == 0 ? F::c[0] + static_cast<float>(S)
+                      : static_cast<float>(static_cast<double>(F::c[i]) * pow2(S * i));
+    return a;
+  }();
+  static constexpr float kP = static_cast<float>(F::p * pow2(S));
+  static constexpr float kScale = static_cast<float>(pow2(S));
   __device__ static float f(float x) {
     const float t = finite_abs(x);
-    const float rs = __builtin_amdgcn_rcpf(
-        fmaf(t, static_cast<float>(F::p * pow2(S)), static_cast<float>(pow2(S))));  // 2^-S r
-    float c = coef(D);
+    const float rs = __builtin_amdgcn_rcpf(fmaf(t, kP, kScale));   // 2^-S r
+    float c = kCoef.c[D];
 #pragma unroll
-    for (int i = D - 1; i >= 0; --i) c = fmaf(c, rs, coef(i));
+    for (int i = D - 1; i >= 0; --i) c = fmaf(c, rs, kCoef.c[i]);
     const float e = __builtin_amdgcn_exp2f(fmaf(x * x, -kHalfLog2e, c));    // 2^S Q(t) / r
     return fmaf(-(t * rs), e, relu(x));   // relu(x) - t Q(t); NaN via x*x
   }
@@ -281,7 +293,8 @@ struct Act<DT, FEWBIT_SILU> {
   static constexpr int S = Prec<DT>::kSiluS;
   __device__ static float f(float x) {
     const float e = __builtin_amdgcn_exp2f(fmaf(fabsf(x), -kLog2e, static_cast<float>(S)));  // 2^S e^-t
-    const float r = __builtin_amdgcn_rcpf(e + static_cast<float>(pow2(S)));  // 1/(2^S (1 + e^-t))
+    constexpr float kScale = static_cast<float>(pow2(S));
+    const float r = __builtin_amdgcn_rcpf(e + kScale);  // 1/(2^S (1 + e^-t))
     return fmaf(-(finite_abs(x) * e), r, relu(x));    // relu(x) - t sigma(-t); NaN via e
   }
 };
@@ -292,8 +305,9 @@ struct Act<DT, FEWBIT_SIGMOID> {
   __device__ static float f(float x) {
     const float t = fabsf(x);
     const float e = __builtin_amdgcn_exp2f(fmaf(t, -kLog2e, static_cast<float>(S)));  // 2^S e^-t
-    const float r = __builtin_amdgcn_rcpf(e + static_cast<float>(pow2(S)));  // 1/(2^S (1 + e^-t))
-    return ((x >= 0.0f) ? static_cast<float>(pow2(S)) : e) * r;   // NaN: e * r is NaN
+    constexpr float kScale = static_cast<float>(pow2(S));
+    const float r = __builtin_amdgcn_rcpf(e + kScale);  // 1/(2^S (1 + e^-t))
+    return ((x >= 0.0f) ? kScale : e) * r;   // NaN: e * r is NaN
   }
 };
 
@@ -783,7 +797,7 @@ template <int DT, int BITS>
 __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
     const void* g, const uint32_t* __restrict__ codes, void* gin, int64_t n, int64_t nwords,
     TableArgs tab) {
-  constexpr int U = FEWBIT_BWD_UNROLL;
+  constexpr int U = (DT == FEWBIT_F32) ? FEWBIT_BWD32_UNROLL : FEWBIT_BWD_UNROLL;
   constexpr int V = Grad<DT, BITS>::kVecs;
   constexpr int kWords = 16 * BITS;
   constexpr int kEsz = (DT == FEWBIT_F32) ? 4 : 2;
