@@ -65,13 +65,13 @@
 #define FEWBIT_FWD16_STREAM_WAVES (FEWBIT_FWD16_THREADS / 64)
 #endif
 #ifndef FEWBIT_FWD32_THREADS
-#define FEWBIT_FWD32_THREADS 512
+#define FEWBIT_FWD32_THREADS 256
 #endif
 #ifndef FEWBIT_FWD32_WG_PER_CU
 #define FEWBIT_FWD32_WG_PER_CU 2
 #endif
 #ifndef FEWBIT_FWD32_UNROLL
-#define FEWBIT_FWD32_UNROLL 1
+#define FEWBIT_FWD32_UNROLL 2
 #endif
 #ifndef FEWBIT_BWD_THREADS
 #define FEWBIT_BWD_THREADS 512
@@ -82,8 +82,8 @@
 #ifndef FEWBIT_BWD_UNROLL
 #define FEWBIT_BWD_UNROLL 4
 #endif
-#ifndef FEWBIT_BWD32_UNROLL             // fp32 tiles are twice the bytes
-#define FEWBIT_BWD32_UNROLL 2
+#ifndef FEWBIT_BWD32_UNROLL             // fp32 tiles are twice the bytes of 16-bit ones
+#define FEWBIT_BWD32_UNROLL 1
 #endif
 #ifndef FEWBIT_NT_LOADS
 #define FEWBIT_NT_LOADS 1             // non-temporal stream loads
@@ -313,7 +313,25 @@ struct Act<DT, FEWBIT_SIGMOID> {
 
 template <int DT>
 struct Act<DT, FEWBIT_TANH> {
-  __device__ static float f(float x) { return tanhf(x); }
+  __device__ static float f(float x) { return tanhf(x); }     // 16-bit tables, built once
+};
+
+// fp32 tanh per element: 1 - 2 / (e^(2|x|) + 1) with the hardware exponential
+// and reciprocal (absolute error about 2^-22), and below |x| = 1/4, where
+// that form loses relative accuracy, the odd Taylor series to x^9 (first
+// omitted term below 1e-8 relative).  The sign is copied from x; NaN and
+// infinities follow from the exponential.
+template <>
+struct Act<FEWBIT_F32, FEWBIT_TANH> {
+  __device__ static float f(float x) {
+    const float t = fabsf(x);
+    const float e = __builtin_amdgcn_exp2f(t * (2.0f * kLog2e));
+    const float big = fmaf(-2.0f, __builtin_amdgcn_rcpf(e + 1.0f), 1.0f);
+    const float z = x * x;
+    const float p = fmaf(z, fmaf(z, fmaf(z, fmaf(z, 62.0f / 2835.0f, -17.0f / 315.0f),
+                                         2.0f / 15.0f), -1.0f / 3.0f), 1.0f);
+    return copysignf(t < 0.25f ? t * p : big, x);
+  }
 };
 
 template <int DT>
@@ -342,12 +360,57 @@ struct Act<DT, FEWBIT_SOFTPLUS> {
 // ---------------------------------------------------------------- classify
 // idx = number of boundaries s[m] <= x: half-open intervals [s[m-1], s[m]).
 // IEEE compares: NaN gives 0, -0 == +0, subnormals are not flushed.
-template <int BITS>
-__device__ inline uint32_t classify(float x, const TableArgs& tab) {
-  uint32_t c = 0;
+//
+// Branch-free binary search over the sorted boundaries: level L tests the
+// boundary s[idx + step - 1] (step = 2^(BITS-1-L)), chosen among the 2^L
+// candidates by the answers of the levels before it (a select tree over
+// scalar-register values), so BITS compares replace 2^BITS - 1.  A NaN fails
+// every test and lands in interval 0, as with the count.
+//
+// The boundaries are first copied to scalar registers through an empty asm
+// barrier: otherwise the compiler turns the selects into indexed loads from
+// the kernel-argument block, a memory load per level and element.
+struct Bounds {
+  float s[15];
+};
+
+__device__ inline Bounds bounds_of(const TableArgs& tab) {
+  Bounds b;
 #pragma unroll
-  for (int m = 0; m < (1 << BITS) - 1; ++m) c += (x >= tab.s[m]) ? 1u : 0u;
-  return c;
+  for (int m = 0; m < 15; ++m) {
+    float t = tab.s[m];
+    asm("" : "+s"(t));
+    b.s[m] = t;
+  }
+  return b;
+}
+
+template <int BITS, int L, int D, int K>
+__device__ inline float pick_boundary(const bool (&c)[BITS], const Bounds& bd) {
+  if constexpr (D == L) {
+    constexpr int step = 1 << (BITS - 1 - L);
+    return bd.s[K * 2 * step + step - 1];
+  } else {
+    return c[D] ? pick_boundary<BITS, L, D + 1, 2 * K + 1>(c, bd)
+                : pick_boundary<BITS, L, D + 1, 2 * K>(c, bd);
+  }
+}
+
+template <int BITS, int L = 0>
+__device__ inline void search_levels(float x, const Bounds& bd, bool (&c)[BITS], uint32_t& idx) {
+  if constexpr (L < BITS) {
+    c[L] = x >= pick_boundary<BITS, L, 0, 0>(c, bd);
+    idx += c[L] ? (1u << (BITS - 1 - L)) : 0u;
+    search_levels<BITS, L + 1>(x, bd, c, idx);
+  }
+}
+
+template <int BITS>
+__device__ inline uint32_t classify(float x, const Bounds& bd) {
+  bool c[BITS] = {};
+  uint32_t idx = 0;
+  search_levels<BITS>(x, bd, c, idx);
+  return idx;
 }
 
 // ---------------------------------------------------------------- packing
@@ -546,9 +609,10 @@ __device__ void build_code_table(uint8_t* clut, const TableArgs& tab, int symmet
   constexpr uint32_t kSeg = 65536u / FEWBIT_FWD16_THREADS;
   static_assert(kSeg >= 32 && kSeg <= 32768 && 65536u % FEWBIT_FWD16_THREADS == 0,
                 "segments of whole 16-byte stores within one sign");
+  const Bounds bd = bounds_of(tab);
   auto code_of = [&](uint32_t p) {
     const float v = Half<DT>::widen(p);
-    return classify<BITS>(symmetric ? fabsf(v) : v, tab);
+    return classify<BITS>(symmetric ? fabsf(v) : v, bd);
   };
   const uint32_t p0 = threadIdx.x * kSeg;
   const uint32_t last = p0 + kSeg - 1u;
@@ -683,16 +747,72 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   }
 }
 
+// ---------------------------------------------------------------- fp32 tiles
+// An fp32 tile is 512 elements in two halves of 256; lane l holds elements
+// 4l .. 4l+3 of each half, so each 16-byte access instruction covers 1 KiB
+// of contiguous memory.  (Eight consecutive elements per lane would need two
+// accesses 32 bytes apart per lane, each instruction touching only every
+// other 16 bytes of its span, which streams far below the contiguous rate.)
+// In stream order a half's codes are then the lanes' fields of 4*BITS bits
+// laid end to end, 8*BITS words per half, 16*BITS per tile.
+template <int BITS>
+struct Codes32 {
+  static constexpr int FB = 4 * BITS;                  // field bits per lane and half
+  static constexpr uint32_t kMask = (1u << FB) - 1u;
+  static constexpr int kHalfWords = 8 * BITS;
+  static constexpr int kWords = 16 * BITS;
+  // most lanes whose fields meet one word: 32 / FB when fields tile words,
+  // else a partial field at each end (for 12-bit fields: 4 lanes)
+  static constexpr int kSources = 32 / FB + ((32 % FB) ? 2 : 0);
+};
+
+// Every lane builds word q = lane mod 16*BITS of the tile from the fields
+// of the lanes it covers (cross-lane reads of f0 | f1 << 16), and stores it;
+// lanes past 16*BITS store identical copies.  FULL: the whole tile exists,
+// so no store is masked off; else only words below `valid` are stored.
+template <int BITS, bool FULL>
+__device__ inline void pack_store32(uint32_t* out, uint32_t f0, uint32_t f1, int lane,
+                                    int64_t valid) {
+  using C = Codes32<BITS>;
+  const uint32_t both = f0 | (f1 << 16);
+  const int q = lane % C::kWords;
+  const int v = q / C::kHalfWords, w = q % C::kHalfWords;
+  const int a = (32 * w) / C::FB, o = (32 * w) % C::FB;
+  uint32_t word = 0;
+#pragma unroll
+  for (int i = 0; i < C::kSources; ++i) {
+    const uint32_t f = (static_cast<uint32_t>(__shfl(static_cast<int>(both), (a + i) & 63)) >>
+                        (16 * v)) & C::kMask;
+    const int sh = i * C::FB - o;                      // bit position of the field in the word
+    word |= (i == 0) ? (f >> o) : (sh < 32 ? f << sh : 0u);
+  }
+  if (FULL || q < valid) st_word(out + q, word);
+}
+
+// The field of lane `lane` in half v: the one or two words it spans,
+// funnel-shifted.  FULL: every word of the tile exists; else words from
+// `valid` on read as 0.
+template <int BITS, bool FULL>
+__device__ inline uint32_t load_field32(const uint32_t* base, int v, int lane, int64_t valid) {
+  using C = Codes32<BITS>;
+  const int b0 = lane * C::FB;
+  const int i0 = v * C::kHalfWords + (b0 >> 5);
+  const int i1 = min(i0 + 1, C::kWords - 1);           // unused unless the field straddles
+  const uint32_t lo = (FULL || i0 < valid) ? ld_word(base + i0) : 0u;
+  const uint32_t hi = (FULL || i1 < valid) ? ld_word(base + i1) : 0u;
+  return __builtin_amdgcn_alignbit(hi, lo, b0 & 31) & C::kMask;
+}
+
 // ---------------------------------------------------------------- forward, fp32
 template <int BITS, int ACT>
-__device__ inline void fwd32_tile(const u32x4_t (&in)[2], const TableArgs& tab, int symmetric,
-                                  u32x4_t (&out)[2], uint32_t& F) {
-  F = 0;
+__device__ inline void fwd32_half(u32x4_t in, const Bounds& bd, int symmetric, u32x4_t& out,
+                                  uint32_t& f) {
+  f = 0;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const float xv = __uint_as_float(in[j >> 2][j & 3]);
-    out[j >> 2][j & 3] = __float_as_uint(Act<FEWBIT_F32, ACT>::f(xv));
-    F |= classify<BITS>(symmetric ? fabsf(xv) : xv, tab) << (BITS * j);
+  for (int j = 0; j < 4; ++j) {
+    const float xv = __uint_as_float(in[j]);
+    out[j] = __float_as_uint(Act<FEWBIT_F32, ACT>::f(xv));
+    f |= classify<BITS>(symmetric ? fabsf(xv) : xv, bd) << (BITS * j);
   }
 }
 
@@ -701,56 +821,60 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
     const float* x, float* y, uint32_t* __restrict__ codes, int64_t n, int64_t nwords,
     TableArgs tab, int symmetric) {
   constexpr int U = FEWBIT_FWD32_UNROLL;
-  constexpr int kWords = 16 * BITS;
+  constexpr int kWords = Codes32<BITS>::kWords;
+  const Bounds bd = bounds_of(tab);
   const WaveIndex wi = wave_index();
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
-  const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
+  const int64_t lane_off = static_cast<int64_t>(wi.lane) * 4;
 
   for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
     const int64_t t0 = gi * U;
     u32x4_t in[U][2], out[U][2];
-    uint32_t F[U];
+    uint32_t f[U][2];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) in[u][h] = ld_stream(x + (t0 + u) * kTile + h * 256 + lane_off);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) fwd32_half<BITS, ACT>(in[u][h], bd, symmetric, out[u][h], f[u][h]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const float* p = x + (t0 + u) * kTile + lane_off;
-      in[u][0] = ld_stream(p);
-      in[u][1] = ld_stream(p + 4);
-    }
 #pragma unroll
-    for (int u = 0; u < U; ++u) fwd32_tile<BITS, ACT>(in[u], tab, symmetric, out[u], F[u]);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float* q = y + (t0 + u) * kTile + lane_off;
-      st_stream(q, out[u][0]);
-      st_stream(q + 4, out[u][1]);
-      pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
+      for (int h = 0; h < 2; ++h) st_stream(y + (t0 + u) * kTile + h * 256 + lane_off, out[u][h]);
+      pack_store32<BITS, true>(codes + (t0 + u) * kWords, f[u][0], f[u][1], wi.lane, kWords);
     }
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
-    const float* p = x + t * kTile + lane_off;
-    const u32x4_t in[2] = {ld_stream(p), ld_stream(p + 4)};
     u32x4_t out[2];
-    uint32_t F;
-    fwd32_tile<BITS, ACT>(in, tab, symmetric, out, F);
-    st_stream(y + t * kTile + lane_off, out[0]);
-    st_stream(y + t * kTile + lane_off + 4, out[1]);
-    pack_store_full<BITS>(codes + t * kWords, F, wi.lane);
+    uint32_t f[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      fwd32_half<BITS, ACT>(ld_stream(x + t * kTile + h * 256 + lane_off), bd, symmetric, out[h],
+                            f[h]);
+      st_stream(y + t * kTile + h * 256 + lane_off, out[h]);
+    }
+    pack_store32<BITS, true>(codes + t * kWords, f[0], f[1], wi.lane, kWords);
   }
+  // the partial tile at the end, if any, goes to the wave that would own it
   if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
     const int64_t t = full;
-    uint32_t F = 0;
+    uint32_t f[2] = {0u, 0u};
 #pragma unroll
-    for (int j = 0; j < kPerLane; ++j) {
-      const int64_t e = t * kTile + lane_off + j;
-      if (e < n) {
-        const float xv = x[e];
-        y[e] = Act<FEWBIT_F32, ACT>::f(xv);
-        F |= classify<BITS>(symmetric ? fabsf(xv) : xv, tab) << (BITS * j);
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t e = t * kTile + h * 256 + lane_off + j;
+        if (e < n) {
+          const float xv = x[e];
+          y[e] = Act<FEWBIT_F32, ACT>::f(xv);
+          f[h] |= classify<BITS>(symmetric ? fabsf(xv) : xv, bd) << (BITS * j);
+        }
       }
-    }
     const int64_t wbase = t * kWords;
-    pack_store<BITS>(codes + wbase, F, wi.lane, nwords - wbase);
+    pack_store32<BITS, false>(codes + wbase, f[0], f[1], wi.lane, nwords - wbase);
   }
 }
 
@@ -778,26 +902,12 @@ struct Grad {
   }
 };
 
-template <int BITS>
-struct Grad<FEWBIT_F32, BITS> {
-  static constexpr int kVecs = 2;
-  __device__ static void apply(const u32x4_t (&g)[2], uint32_t F, const f32x2_t* pairs,
-                               u32x4_t (&out)[2]) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const f32x2_t v = pair_values<BITS>(pairs, F, k);
-      const int a = 2 * k, b = 2 * k + 1;
-      out[a >> 2][a & 3] = __float_as_uint(__uint_as_float(g[a >> 2][a & 3]) * v.x);
-      out[b >> 2][b & 3] = __float_as_uint(__uint_as_float(g[b >> 2][b & 3]) * v.y);
-    }
-  }
-};
-
 template <int DT, int BITS>
 __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
     const void* g, const uint32_t* __restrict__ codes, void* gin, int64_t n, int64_t nwords,
     TableArgs tab) {
-  constexpr int U = (DT == FEWBIT_F32) ? FEWBIT_BWD32_UNROLL : FEWBIT_BWD_UNROLL;
+  static_assert(DT != FEWBIT_F32, "fp32 uses bwd32_kernel");
+  constexpr int U = FEWBIT_BWD_UNROLL;
   constexpr int V = Grad<DT, BITS>::kVecs;
   constexpr int kWords = 16 * BITS;
   constexpr int kEsz = (DT == FEWBIT_F32) ? 4 : 2;
@@ -856,6 +966,78 @@ __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
       const int64_t e = t * kTile + lane_off + j;
       if (e < n)
         Scalar<DT>::store(gin, e, Scalar<DT>::load(g, e) * val[2 * ((F >> (BITS * j)) & kMask)]);
+    }
+  }
+}
+
+// fp32 backward on the fp32 tile layout (see fp32 tiles above).
+template <int BITS>
+__device__ inline u32x4_t grad32_half(u32x4_t g, uint32_t f, const f32x2_t* pairs) {
+  u32x4_t out;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const f32x2_t v = pair_values<BITS>(pairs, f, k);
+    out[2 * k] = __float_as_uint(__uint_as_float(g[2 * k]) * v.x);
+    out[2 * k + 1] = __float_as_uint(__uint_as_float(g[2 * k + 1]) * v.y);
+  }
+  return out;
+}
+
+template <int BITS>
+__global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd32_kernel(
+    const float* g, const uint32_t* __restrict__ codes, float* gin, int64_t n, int64_t nwords,
+    TableArgs tab) {
+  constexpr int U = FEWBIT_BWD32_UNROLL;
+  constexpr int kWords = Codes32<BITS>::kWords;
+  constexpr uint32_t kMask = (1u << BITS) - 1u;
+  constexpr int kPairs = 1 << (2 * BITS);
+  __shared__ f32x2_t pairs[kPairs];
+  for (int i = threadIdx.x; i < kPairs; i += blockDim.x)
+    pairs[i] = (f32x2_t){tab.v[i & kMask], tab.v[i >> BITS]};
+  __syncthreads();
+  const float* val = reinterpret_cast<const float*>(pairs);   // val[2c] = v[c] (c < K)
+
+  const WaveIndex wi = wave_index();
+  const int64_t full = n / kTile;
+  const int64_t groups = full / U;
+  const int64_t lane_off = static_cast<int64_t>(wi.lane) * 4;
+
+  for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
+    const int64_t t0 = gi * U;
+    u32x4_t in[U][2];
+    uint32_t f[U][2];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        in[u][h] = ld_stream(g + (t0 + u) * kTile + h * 256 + lane_off);
+        f[u][h] = load_field32<BITS, true>(codes + (t0 + u) * kWords, h, wi.lane, kWords);
+      }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        st_stream(gin + (t0 + u) * kTile + h * 256 + lane_off, grad32_half<BITS>(in[u][h], f[u][h], pairs));
+  }
+  for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const u32x4_t in = ld_stream(g + t * kTile + h * 256 + lane_off);
+      const uint32_t f = load_field32<BITS, true>(codes + t * kWords, h, wi.lane, kWords);
+      st_stream(gin + t * kTile + h * 256 + lane_off, grad32_half<BITS>(in, f, pairs));
+    }
+  }
+  if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
+    const int64_t t = full;
+    const int64_t wbase = t * kWords;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t f = load_field32<BITS, false>(codes + wbase, h, wi.lane, nwords - wbase);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t e = t * kTile + h * 256 + lane_off + j;
+        if (e < n) gin[e] = g[e] * val[2 * ((f >> (BITS * j)) & kMask)];
+      }
     }
   }
 }
@@ -1003,8 +1185,13 @@ void launch_bwd(const Launch& L) {
   const int64_t nw = (L.n * BITS + 31) / 32;
   const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS / kWave, FEWBIT_BWD_WG_PER_CU);
   (void)hipGetLastError();
-  hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s, L.in,
-                     L.codes, L.out, L.n, nw, table_args(L.t));
+  if constexpr (DT == FEWBIT_F32)
+    hipLaunchKernelGGL((bwd32_kernel<BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s,
+                       static_cast<const float*>(L.in), L.codes, static_cast<float*>(L.out), L.n,
+                       nw, table_args(L.t));
+  else
+    hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s, L.in,
+                       L.codes, L.out, L.n, nw, table_args(L.t));
 }
 
 template <int DT>
