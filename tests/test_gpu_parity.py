@@ -278,6 +278,56 @@ def test_side_stream():
     check_y(download(y, "bf16"), y_ref, "bf16", "stream y")
 
 
+def _codes_at(codes_dev, idx, bits):
+    """Codes of elements idx from the packed device buffer (fetching only
+    the words they touch), by the stream layout: bit t of code i is stream
+    bit bits*i + t, in word p / 32 at bit p % 32."""
+    first = (idx * bits) // 32
+    words = torch.stack([codes_dev[torch.from_numpy(first).cuda()],
+                         codes_dev[torch.from_numpy(np.minimum(first + 1, codes_dev.numel() - 1)).cuda()]])
+    w = words.cpu().numpy().view(np.uint32).astype(np.uint64)
+    both = w[0] | (w[1] << np.uint64(32))
+    return ((both >> ((idx * bits) % 32).astype(np.uint64)) & np.uint64((1 << bits) - 1)).astype(np.int64)
+
+
+@pytest.mark.slow
+def test_beyond_two_to_the_31_elements():
+    # 64-bit element, tile and word indexing: a bf16 tensor of 2^31 + 12345
+    # elements (about 18 GB resident with outputs and gradients), checked at
+    # sampled positions around 2^31, at the end and at random, against the
+    # oracle evaluated on those elements alone
+    n = (1 << 31) + 12345
+    key = "gelu_bf16_lm_ffn_16x2048x8192/b3"
+    spec, table = golden_table(key)
+    bits = spec["bits"]
+    s = np.float32([float.fromhex(h) for h in spec["s"]])
+    v = np.float32([float.fromhex(h) for h in spec["v"]])
+    print(f"[big] n={n}", flush=True)
+    gen = torch.Generator(device="cuda").manual_seed(41)
+    x = (torch.randn(n, device="cuda", generator=gen) * 3).to(torch.bfloat16)
+    g = torch.randn(n, device="cuda", generator=gen).to(torch.bfloat16)
+    y, codes = P.fwd(table, x)
+    gin = P.bwd(table, g, codes)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(42)
+    idx = np.unique(np.concatenate([
+        np.arange((1 << 31) - 3000, (1 << 31) + 3000), np.arange(n - 5000, n),
+        rng.integers(0, n, 200000)]))
+    it = torch.from_numpy(idx).cuda()
+    xs = x[it].view(torch.int16).cpu().numpy().view(np.uint16)
+    gs = g[it].view(torch.int16).cpu().numpy().view(np.uint16)
+    ys = y[it].view(torch.int16).cpu().numpy().view(np.uint16)
+    gis = gin[it].view(torch.int16).cpu().numpy().view(np.uint16)
+    y_ref, c_packed = O.fwd(O.GELU, O.BF16, bits, s, xs)
+    idx_ref = O.unpack(c_packed, xs.size, bits)
+    check_y(ys, y_ref, "bf16", "y sampled")
+    check_exact(_codes_at(codes, idx, bits), idx_ref.astype(np.int64), "codes sampled")
+    gin_ref = O.bwd(O.BF16, bits, v, gs, c_packed)
+    check_exact(gis, gin_ref, "grad_in sampled")
+    del x, g, y, codes, gin
+    torch.cuda.empty_cache()
+
+
 def test_graph_capture_replays():
     # forward + backward captured into a graph after one eager call (which
     # builds the per-device output tables), replayed several times with
