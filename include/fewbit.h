@@ -14,6 +14,8 @@
  * Conventions for every entry point:
  *   - Plain C types only.  Device pointers are HIP device addresses; the
  *     stream argument is a hipStream_t passed as void* (NULL = null stream).
+ *   - Device: the current HIP device must own the buffers and the stream;
+ *     fwd / bwd reject a stream of another device with FEWBIT_E_INVALID.
  *   - The caller owns every buffer.  The library never allocates or frees
  *     device memory and never synchronises the caller's streams.
  *   - All argument checks run on the host before anything is launched, so a

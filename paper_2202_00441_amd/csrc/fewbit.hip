@@ -54,11 +54,6 @@
 #ifndef FEWBIT_FWD16_UNROLL
 #define FEWBIT_FWD16_UNROLL 4
 #endif
-// 1: the fp16 / bf16 forward loads the next group of tiles before it looks
-// up the current one, so loads stay in flight during the LDS lookups
-#ifndef FEWBIT_FWD16_PIPELINE
-#define FEWBIT_FWD16_PIPELINE 0
-#endif
 // waves per fp16 / bf16 forward workgroup that stream after the tables are
 // built (all of them build the tables; the rest then exit)
 #ifndef FEWBIT_FWD16_STREAM_WAVES
@@ -682,44 +677,18 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
 
-  if constexpr (FEWBIT_FWD16_PIPELINE) {
-    u32x4_t in[U];
-    if (wi.wave < groups) {
+  for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
+    const int64_t t0 = gi * U;
+    u32x4_t in[U], out[U];
+    uint32_t F[U];
 #pragma unroll
-      for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (wi.wave * U + u) * kTile + lane_off);
-    }
-    for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
-      const int64_t t0 = gi * U, next = gi + wi.nwaves;
-      u32x4_t nx[U], out[U];
-      uint32_t F[U];
-      if (next < groups) {      // the same for the whole wave
+    for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (t0 + u) * kTile + lane_off);
 #pragma unroll
-        for (int u = 0; u < U; ++u) nx[u] = ld_stream(x + (next * U + u) * kTile + lane_off);
-      }
+    for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
 #pragma unroll
-      for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
-        pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) in[u] = nx[u];
-    }
-  } else {
-    for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
-      const int64_t t0 = gi * U;
-      u32x4_t in[U], out[U];
-      uint32_t F[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (t0 + u) * kTile + lane_off);
-#pragma unroll
-      for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
-        pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
-      }
+    for (int u = 0; u < U; ++u) {
+      st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
+      pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
     }
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
@@ -1129,6 +1098,16 @@ int ensure_output_tables() {
   return FEWBIT_OK;
 }
 
+// The stream must belong to the current device: the grid size, the output
+// tables and the launch all refer to the current device.
+int check_stream_device(hipStream_t stream) {
+  int current = 0;
+  hipDevice_t owner = 0;
+  if (hipGetDevice(&current) != hipSuccess || hipStreamGetDevice(stream, &owner) != hipSuccess)
+    return FEWBIT_E_HIP;
+  return owner == current ? FEWBIT_OK : FEWBIT_E_INVALID;
+}
+
 struct Launch {
   const fewbit_table* t;
   const void* in;
@@ -1227,6 +1206,8 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   if (n == 0) return FEWBIT_OK;
   if (!x || !y || !codes) return FEWBIT_E_NULL;
   if (misaligned(x) || misaligned(y) || misaligned(codes)) return FEWBIT_E_ALIGN;
+  rc = check_stream_device(static_cast<hipStream_t>(stream));
+  if (rc != FEWBIT_OK) return rc;
   if (dtype != FEWBIT_F32) {
     rc = ensure_output_tables();
     if (rc != FEWBIT_OK) return rc;
@@ -1249,6 +1230,8 @@ extern "C" int fewbit_bwd(const fewbit_table* t, int32_t dtype, const void* grad
   if (n == 0) return FEWBIT_OK;
   if (!grad_out || !codes || !grad_in) return FEWBIT_E_NULL;
   if (misaligned(grad_out) || misaligned(codes) || misaligned(grad_in)) return FEWBIT_E_ALIGN;
+  rc = check_stream_device(static_cast<hipStream_t>(stream));
+  if (rc != FEWBIT_OK) return rc;
   const Launch L{t, grad_out, grad_in, const_cast<uint32_t*>(codes), n,
                  static_cast<hipStream_t>(stream)};
   switch (dtype) {
