@@ -58,14 +58,14 @@ def measured_traffic(workload: str, bits: int, kernel: str):
 
 # ---------------------------------------------------------------- rocprofv3 summaries
 DT_NAMES = {0: "f32", 1: "f16", 2: "bf16"}
-ACT_NAMES = {0: "gelu", 1: "silu", 2: "sigmoid", 3: "tanh"}
+ACT_NAMES = {0: "gelu", 1: "silu", 2: "sigmoid", 3: "tanh", 4: "relu", 5: "selu", 6: "softplus"}
 
 
 def _kernel_key(name: str):
     """'fwd16_kernel<bf16,3,gelu>' style key of a library kernel named in a
     rocprofv3 csv, or the plain name for any other kernel."""
     import re
-    m = re.search(r"(fwd16_kernel|fwd32_kernel|bwd_kernel)<([0-9, ]+)>", name)
+    m = re.search(r"(fwd16_kernel|fwd32_kernel|bwd32_kernel|bwd_kernel)<([0-9, ]+)>", name)
     if not m:
         base = name.replace("(anonymous namespace)::", "").replace("void ", "")
         return base.split("(")[0].strip() or name
@@ -74,6 +74,8 @@ def _kernel_key(name: str):
         return f"fwd16_kernel<{DT_NAMES[args[0]]},{args[1]},{ACT_NAMES[args[2]]}>"
     if m.group(1) == "fwd32_kernel":
         return f"fwd32_kernel<f32,{args[0]},{ACT_NAMES[args[1]]}>"
+    if m.group(1) == "bwd32_kernel":
+        return f"bwd32_kernel<f32,{args[0]}>"
     return f"bwd_kernel<{DT_NAMES[args[0]]},{args[1]}>"
 
 
