@@ -7,13 +7,17 @@
 // backward): grad_in = grad_out * v[idx].
 //
 // Both passes are pointwise and bound by HBM bandwidth.  Work is cut into
-// wave tiles of 512 consecutive elements: each of the 64 lanes of a wave
-// owns 8 consecutive elements (one 16-byte access for fp16/bf16, two for
-// fp32).  Eight codes of b bits make a b-byte field per lane, so the codes
-// of a tile are exactly 16*b whole words and the fields of 4 neighbouring
-// lanes (one DPP quad) always cover whole words: lanes combine their fields
-// with quad permutes instead of atomics or shared memory, and every packed
-// word has exactly one writer.
+// wave tiles of 512 consecutive elements, whose codes are exactly 16*b whole
+// words, and every 16-byte access instruction of a wave covers 1 KiB of
+// contiguous memory.  fp16 / bf16: each lane owns 8 consecutive elements
+// (one 16-byte access); their 8 codes make a b-byte field, and the fields
+// of 4 neighbouring lanes (one DPP quad) always cover whole words, so lanes
+// combine fields with quad permutes instead of atomics or shared memory.
+// fp32: a tile is two halves of 256 and each lane owns 4 consecutive
+// elements of each half (one 16-byte access per half); the words are then
+// gathered from 4b-bit lane fields by cross-lane reads (see fp32 tiles).
+// Each packed word has one value, written by its lane (and by lanes that
+// store an identical copy, so that full tiles need no masking).
 //
 // Streams are read and written with non-temporal 16-byte accesses (nothing
 // is reused), by a grid sized to the device's compute units so each wave
@@ -90,7 +94,7 @@
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kPerLane = 8;                 // elements per lane per tile
+constexpr int kPerLane = 8;                 // elements per lane per 16-bit tile
 constexpr int kTile = kWave * kPerLane;     // 512 elements per wave tile
 
 struct TableArgs {
@@ -153,7 +157,7 @@ struct Half<FEWBIT_F16> {
   static constexpr uint32_t kSpecialFrom = 0x7C00u;
 };
 
-// element-wise access for the partial tile at the end
+// element-wise access to 16-bit data for the partial tile at the end
 template <int DT>
 struct Scalar {
   __device__ static float load(const void* p, int64_t e) {
@@ -162,11 +166,6 @@ struct Scalar {
   __device__ static void store(void* p, int64_t e, float v) {
     static_cast<uint16_t*>(p)[e] = static_cast<uint16_t>(Half<DT>::pack(v, 0.0f) & 0xFFFFu);
   }
-};
-template <>
-struct Scalar<FEWBIT_F32> {
-  __device__ static float load(const void* p, int64_t e) { return static_cast<const float*>(p)[e]; }
-  __device__ static void store(void* p, int64_t e, float v) { static_cast<float*>(p)[e] = v; }
 };
 
 // ---------------------------------------------------------------- activations
