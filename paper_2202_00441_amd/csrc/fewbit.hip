@@ -45,10 +45,15 @@
 #include "../../include/fewbit.h"
 
 // Launch-shape knobs (compile time): threads per workgroup, workgroups per
-// CU (the grid is capped at that many per compute unit and waves then walk
-// the tiles) and tiles in flight per wave, per kernel.  The fp16 / bf16
-// forward holds 160 KiB of tables per workgroup (all of a CU's LDS), so one
-// workgroup fits per CU.
+// CU and tiles per wave and loop trip, per kernel.  A positive WG_PER_CU
+// caps the grid at that many workgroups per compute unit, and waves then walk
+// the tiles (persistent); 0 launches one wave per tile group, and the
+// hardware dispatcher hands out workgroups as earlier ones finish.  The
+// dispatcher balances the load between compute units, whose streaming rates
+// differ by a few per cent from one to another; a persistent grid ends only
+// when its slowest unit has walked its share.  The fp16 / bf16 forward holds
+// 160 KiB of tables per workgroup (all of a CU's LDS), built at its start, so
+// it is persistent with one workgroup per CU.
 #ifndef FEWBIT_FWD16_THREADS
 #define FEWBIT_FWD16_THREADS 512
 #endif
@@ -67,21 +72,21 @@
 #define FEWBIT_FWD32_THREADS 256
 #endif
 #ifndef FEWBIT_FWD32_WG_PER_CU
-#define FEWBIT_FWD32_WG_PER_CU 2
+#define FEWBIT_FWD32_WG_PER_CU 0
 #endif
 #ifndef FEWBIT_FWD32_UNROLL
-#define FEWBIT_FWD32_UNROLL 2
+#define FEWBIT_FWD32_UNROLL 1
 #endif
 #ifndef FEWBIT_BWD_THREADS
-#define FEWBIT_BWD_THREADS 512
+#define FEWBIT_BWD_THREADS 64
 #endif
 #ifndef FEWBIT_BWD_WG_PER_CU
-#define FEWBIT_BWD_WG_PER_CU 1
+#define FEWBIT_BWD_WG_PER_CU 0
 #endif
 #ifndef FEWBIT_BWD_UNROLL
-#define FEWBIT_BWD_UNROLL 4
+#define FEWBIT_BWD_UNROLL 1
 #endif
-#ifndef FEWBIT_BWD32_UNROLL             // fp32 tiles are twice the bytes of 16-bit ones
+#ifndef FEWBIT_BWD32_UNROLL
 #define FEWBIT_BWD32_UNROLL 1
 #endif
 #ifndef FEWBIT_NT_LOADS
@@ -96,6 +101,8 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kPerLane = 8;                 // elements per lane per 16-bit tile
 constexpr int kTile = kWave * kPerLane;     // 512 elements per wave tile
+constexpr uint32_t kLaneBytes = 16;         // one 16-byte access per lane and instruction
+constexpr uint32_t kSpanBytes = kWave * kLaneBytes;   // 1 KiB per wave instruction
 
 struct TableArgs {
   float s[15];
@@ -107,14 +114,34 @@ typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ inline u32x4_t ld_stream(const void* p) {
-  if constexpr (FEWBIT_NT_LOADS) return __builtin_nontemporal_load(static_cast<const u32x4_t*>(p));
-  return *static_cast<const u32x4_t*>(p);
-}
-__device__ inline void st_stream(void* p, u32x4_t v) {
-  if constexpr (FEWBIT_NT_STORES) __builtin_nontemporal_store(v, static_cast<u32x4_t*>(p));
-  else *static_cast<u32x4_t*>(p) = v;
-}
+// Stream accesses go through buffer instructions on a wave-uniform span: a
+// resource descriptor for `bytes` bytes from a wave-uniform address (scalar
+// registers), plus a per-lane byte offset.  The cache policy is explicit in
+// every instruction (the non-temporal hint of plain loads and stores can be
+// dropped by the compiler when it merges or moves them), and the hardware
+// range check turns any access at or past `bytes` into a zero load or a
+// dropped store.  Cache-policy bits: 2 = nt (streaming, not kept in cache).
+constexpr int kLoadPolicy = FEWBIT_NT_LOADS ? 2 : 0;
+constexpr int kStorePolicy = FEWBIT_NT_STORES ? 2 : 0;
+
+struct Span {
+  __amdgpu_buffer_rsrc_t r;
+  // 0x00020000: raw (unformatted) 32-bit buffer accesses on gfx9
+  __device__ Span(const void* base, uint32_t bytes)
+      : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000)) {}
+  __device__ u32x4_t ld16(uint32_t off) const {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kLoadPolicy);
+  }
+  __device__ void st16(uint32_t off, u32x4_t v) const {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kStorePolicy);
+  }
+  __device__ uint32_t ld4(uint32_t off) const {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kLoadPolicy);
+  }
+  __device__ void st4(uint32_t off, uint32_t v) const {
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, kStorePolicy);
+  }
+};
 
 // ---------------------------------------------------------------- storage
 // Half types: two elements per 32-bit word, element 2k in the low half.
@@ -416,14 +443,9 @@ __device__ inline uint32_t quad_read(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), CTRL, 0xF, 0xF, false));
 }
 
-__device__ inline void st_word(uint32_t* p, uint32_t v) {
-  if constexpr (FEWBIT_NT_STORES) __builtin_nontemporal_store(v, p);
-  else *p = v;
-}
-__device__ inline uint32_t ld_word(const uint32_t* p) {
-  if constexpr (FEWBIT_NT_LOADS) return __builtin_nontemporal_load(p);
-  return *p;
-}
+// word i of a code span
+__device__ inline void st_word(const Span& c, int i, uint32_t v) { c.st4(static_cast<uint32_t>(i) * 4u, v); }
+__device__ inline uint32_t ld_word(const Span& c, int i) { return c.ld4(static_cast<uint32_t>(i) * 4u); }
 
 // Lane field F holds the 8 codes of the lane (8*BITS bits, code j at bit
 // BITS*j).  The tile's stream is the lane fields laid end to end, so lane l's
@@ -431,27 +453,27 @@ __device__ inline uint32_t ld_word(const uint32_t* p) {
 // index is below `valid` (the rest belong past the end of the buffer).
 // Must be called by all 64 lanes together.
 template <int BITS>
-__device__ inline void pack_store(uint32_t* out, uint32_t F, int lane, int64_t valid) {
+__device__ inline void pack_store(const Span& out, uint32_t F, int lane, int64_t valid) {
   if constexpr (BITS == 4) {
-    if (lane < valid) st_word(out + lane, F);
+    if (lane < valid) st_word(out, lane, F);
   } else if constexpr (BITS == 2) {
     const uint32_t nb = quad_read<quad_perm(1, 1, 3, 3)>(F);
     const uint32_t w = F | (nb << 16);
     const int widx = lane >> 1;
-    if (!(lane & 1) && widx < valid) st_word(out + widx, w);
+    if (!(lane & 1) && widx < valid) st_word(out, widx, w);
   } else if constexpr (BITS == 1) {
     const uint32_t n1 = quad_read<quad_perm(1, 1, 3, 3)>(F);
     const uint32_t a = F | (n1 << 8);
     const uint32_t n2 = quad_read<quad_perm(2, 2, 2, 2)>(a);
     const uint32_t w = a | (n2 << 16);
     const int widx = lane >> 2;
-    if (!(lane & 3) && widx < valid) st_word(out + widx, w);
+    if (!(lane & 3) && widx < valid) st_word(out, widx, w);
   } else {  // BITS == 3: a quad's 4 x 24 bits are words 3q, 3q+1, 3q+2
     const uint32_t nx = quad_read<quad_perm(1, 2, 3, 3)>(F);
     const int k = lane & 3;
     const uint32_t w = (F >> (8 * k)) | (nx << (24 - 8 * k));
     const int widx = 3 * (lane >> 2) + k;
-    if (k < 3 && widx < valid) st_word(out + widx, w);
+    if (k < 3 && widx < valid) st_word(out, widx, w);
   }
 }
 
@@ -462,17 +484,17 @@ __device__ inline void pack_store(uint32_t* out, uint32_t F, int lane, int64_t v
 // it from the quad and funnel-shifts its 24 bits out.  Must be called by all
 // 64 lanes together.
 template <int BITS>
-__device__ inline uint32_t load_field(const uint32_t* base, int lane, int64_t valid) {
+__device__ inline uint32_t load_field(const Span& base, int lane, int64_t valid) {
   if constexpr (BITS == 3) {
     const int k = lane & 3;
     const int widx = 3 * (lane >> 2) + k;
-    const uint32_t w = (k < 3 && widx < valid) ? ld_word(base + widx) : 0u;
+    const uint32_t w = (k < 3 && widx < valid) ? ld_word(base, widx) : 0u;
     const uint32_t prev = quad_read<quad_perm(0, 0, 1, 2)>(w);   // word k-1 (k = 0: word 0)
     const uint32_t own = quad_read<quad_perm(0, 1, 2, 2)>(w);    // word k (k = 3: word 2)
     return __builtin_amdgcn_alignbit(own, prev, (24 * k) & 31);
   } else {
     const int widx = (8 * BITS * lane) >> 5;
-    const uint32_t v = (widx < valid) ? ld_word(base + widx) : 0u;
+    const uint32_t v = (widx < valid) ? ld_word(base, widx) : 0u;
     return v >> ((8 * BITS * lane) & 31);
   }
 }
@@ -484,35 +506,35 @@ __device__ inline uint32_t load_field(const uint32_t* base, int lane, int64_t va
 // neighbour's word to the same address; when unpacking, lane 3 of each quad
 // reloads word 2 of the quad, which the permutes never read.
 template <int BITS>
-__device__ inline void pack_store_full(uint32_t* out, uint32_t F, int lane) {
+__device__ inline void pack_store_full(const Span& out, uint32_t F, int lane) {
   if constexpr (BITS == 4) {
-    st_word(out + lane, F);
+    st_word(out, lane, F);
   } else if constexpr (BITS == 2) {
     const uint32_t lo = quad_read<quad_perm(0, 0, 2, 2)>(F);
     const uint32_t hi = quad_read<quad_perm(1, 1, 3, 3)>(F);
-    st_word(out + (lane >> 1), lo | (hi << 16));
+    st_word(out, lane >> 1, lo | (hi << 16));
   } else if constexpr (BITS == 1) {
     const uint32_t a = quad_read<quad_perm(0, 0, 2, 2)>(F) | (quad_read<quad_perm(1, 1, 3, 3)>(F) << 8);
     const uint32_t w = quad_read<quad_perm(0, 0, 0, 0)>(a) | (quad_read<quad_perm(2, 2, 2, 2)>(a) << 16);
-    st_word(out + (lane >> 2), w);
+    st_word(out, lane >> 2, w);
   } else {  // BITS == 3: lane k of a quad writes word min(k, 2) of the quad
     const int j = min(lane & 3, 2);
     const uint32_t lo = quad_read<quad_perm(0, 1, 2, 2)>(F);
     const uint32_t hi = quad_read<quad_perm(1, 2, 3, 3)>(F);
-    st_word(out + 3 * (lane >> 2) + j, (lo >> (8 * j)) | (hi << (24 - 8 * j)));
+    st_word(out, 3 * (lane >> 2) + j, (lo >> (8 * j)) | (hi << (24 - 8 * j)));
   }
 }
 
 template <int BITS>
-__device__ inline uint32_t load_field_full(const uint32_t* base, int lane) {
+__device__ inline uint32_t load_field_full(const Span& base, int lane) {
   if constexpr (BITS == 3) {
     const int k = lane & 3;
-    const uint32_t w = ld_word(base + 3 * (lane >> 2) + min(k, 2));
+    const uint32_t w = ld_word(base, 3 * (lane >> 2) + min(k, 2));
     const uint32_t prev = quad_read<quad_perm(0, 0, 1, 2)>(w);   // word k-1 (k = 0: word 0)
     const uint32_t own = quad_read<quad_perm(0, 1, 2, 2)>(w);    // word k (k = 3: word 2)
     return __builtin_amdgcn_alignbit(own, prev, (24 * k) & 31);
   } else {
-    return ld_word(base + ((8 * BITS * lane) >> 5)) >> ((8 * BITS * lane) & 31);
+    return ld_word(base, (8 * BITS * lane) >> 5) >> ((8 * BITS * lane) & 31);
   }
 }
 
@@ -522,11 +544,18 @@ struct WaveIndex {
 };
 // Waves 0 .. per_block-1 of every workgroup, numbered across the grid.
 __device__ inline WaveIndex wave_index_of(int per_block) {
+  // the wave's number within its workgroup is the same in all its lanes;
+  // readfirstlane tells the compiler so, which keeps tile addresses scalar
+  const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
   return {static_cast<int>(threadIdx.x & (kWave - 1)),
-          static_cast<int64_t>(blockIdx.x) * per_block + (threadIdx.x / kWave),
+          static_cast<int64_t>(blockIdx.x) * per_block + w,
           static_cast<int64_t>(gridDim.x) * per_block};
 }
-__device__ inline WaveIndex wave_index() { return wave_index_of(blockDim.x / kWave); }
+// The launch's waves per workgroup as a compile-time constant: blockDim
+// would be a vector load from the dispatch packet, waited for before the
+// first stream load.
+template <int THREADS>
+__device__ inline WaveIndex wave_index() { return wave_index_of(THREADS / kWave); }
 
 // ---------------------------------------------------------------- forward, fp16 / bf16
 // For 16-bit inputs both results of the forward are functions of the input
@@ -675,27 +704,28 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
+  const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
 
   for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
     const int64_t t0 = gi * U;
     u32x4_t in[U], out[U];
     uint32_t F[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) in[u] = ld_stream(x + (t0 + u) * kTile + lane_off);
+    for (int u = 0; u < U; ++u) in[u] = Span(x + (t0 + u) * kTile, kSpanBytes).ld16(lane_b);
 #pragma unroll
     for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      st_stream(y + (t0 + u) * kTile + lane_off, out[u]);
-      pack_store_full<BITS>(codes + (t0 + u) * kWords, F[u], wi.lane);
+      Span(y + (t0 + u) * kTile, kSpanBytes).st16(lane_b, out[u]);
+      pack_store_full<BITS>(Span(codes + (t0 + u) * kWords, kWords * 4), F[u], wi.lane);
     }
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
     u32x4_t out;
     uint32_t F;
-    fwd16_tile<BITS>(ld_stream(x + t * kTile + lane_off), ylut, clut, out, F);
-    st_stream(y + t * kTile + lane_off, out);
-    pack_store_full<BITS>(codes + t * kWords, F, wi.lane);
+    fwd16_tile<BITS>(Span(x + t * kTile, kSpanBytes).ld16(lane_b), ylut, clut, out, F);
+    Span(y + t * kTile, kSpanBytes).st16(lane_b, out);
+    pack_store_full<BITS>(Span(codes + t * kWords, kWords * 4), F, wi.lane);
   }
   // the partial tile at the end, if any, goes to the wave that would own it
   if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
@@ -711,7 +741,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
       }
     }
     const int64_t wbase = t * kWords;
-    pack_store<BITS>(codes + wbase, F, wi.lane, nwords - wbase);
+    pack_store<BITS>(Span(codes + wbase, kWords * 4), F, wi.lane, nwords - wbase);
   }
 }
 
@@ -739,7 +769,7 @@ struct Codes32 {
 // lanes past 16*BITS store identical copies.  FULL: the whole tile exists,
 // so no store is masked off; else only words below `valid` are stored.
 template <int BITS, bool FULL>
-__device__ inline void pack_store32(uint32_t* out, uint32_t f0, uint32_t f1, int lane,
+__device__ inline void pack_store32(const Span& out, uint32_t f0, uint32_t f1, int lane,
                                     int64_t valid) {
   using C = Codes32<BITS>;
   const uint32_t both = f0 | (f1 << 16);
@@ -754,20 +784,20 @@ __device__ inline void pack_store32(uint32_t* out, uint32_t f0, uint32_t f1, int
     const int sh = i * C::FB - o;                      // bit position of the field in the word
     word |= (i == 0) ? (f >> o) : (sh < 32 ? f << sh : 0u);
   }
-  if (FULL || q < valid) st_word(out + q, word);
+  if (FULL || q < valid) st_word(out, q, word);
 }
 
 // The field of lane `lane` in half v: the one or two words it spans,
 // funnel-shifted.  FULL: every word of the tile exists; else words from
 // `valid` on read as 0.
 template <int BITS, bool FULL>
-__device__ inline uint32_t load_field32(const uint32_t* base, int v, int lane, int64_t valid) {
+__device__ inline uint32_t load_field32(const Span& base, int v, int lane, int64_t valid) {
   using C = Codes32<BITS>;
   const int b0 = lane * C::FB;
   const int i0 = v * C::kHalfWords + (b0 >> 5);
   const int i1 = min(i0 + 1, C::kWords - 1);           // unused unless the field straddles
-  const uint32_t lo = (FULL || i0 < valid) ? ld_word(base + i0) : 0u;
-  const uint32_t hi = (FULL || i1 < valid) ? ld_word(base + i1) : 0u;
+  const uint32_t lo = (FULL || i0 < valid) ? ld_word(base, i0) : 0u;
+  const uint32_t hi = (FULL || i1 < valid) ? ld_word(base, i1) : 0u;
   return __builtin_amdgcn_alignbit(hi, lo, b0 & 31) & C::kMask;
 }
 
@@ -791,10 +821,11 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
   constexpr int U = FEWBIT_FWD32_UNROLL;
   constexpr int kWords = Codes32<BITS>::kWords;
   const Bounds bd = bounds_of(tab);
-  const WaveIndex wi = wave_index();
+  const WaveIndex wi = wave_index<FEWBIT_FWD32_THREADS>();
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * 4;
+  const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
 
   for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
     const int64_t t0 = gi * U;
@@ -803,7 +834,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) in[u][h] = ld_stream(x + (t0 + u) * kTile + h * 256 + lane_off);
+      for (int h = 0; h < 2; ++h) in[u][h] = Span(x + (t0 + u) * kTile + h * 256, kSpanBytes).ld16(lane_b);
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -811,8 +842,8 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) st_stream(y + (t0 + u) * kTile + h * 256 + lane_off, out[u][h]);
-      pack_store32<BITS, true>(codes + (t0 + u) * kWords, f[u][0], f[u][1], wi.lane, kWords);
+      for (int h = 0; h < 2; ++h) Span(y + (t0 + u) * kTile + h * 256, kSpanBytes).st16(lane_b, out[u][h]);
+      pack_store32<BITS, true>(Span(codes + (t0 + u) * kWords, kWords * 4), f[u][0], f[u][1], wi.lane, kWords);
     }
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
@@ -820,11 +851,11 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
     uint32_t f[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      fwd32_half<BITS, ACT>(ld_stream(x + t * kTile + h * 256 + lane_off), bd, symmetric, out[h],
-                            f[h]);
-      st_stream(y + t * kTile + h * 256 + lane_off, out[h]);
+      fwd32_half<BITS, ACT>(Span(x + t * kTile + h * 256, kSpanBytes).ld16(lane_b), bd, symmetric,
+                            out[h], f[h]);
+      Span(y + t * kTile + h * 256, kSpanBytes).st16(lane_b, out[h]);
     }
-    pack_store32<BITS, true>(codes + t * kWords, f[0], f[1], wi.lane, kWords);
+    pack_store32<BITS, true>(Span(codes + t * kWords, kWords * 4), f[0], f[1], wi.lane, kWords);
   }
   // the partial tile at the end, if any, goes to the wave that would own it
   if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
@@ -842,112 +873,112 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
         }
       }
     const int64_t wbase = t * kWords;
-    pack_store32<BITS, false>(codes + wbase, f[0], f[1], wi.lane, nwords - wbase);
+    pack_store32<BITS, false>(Span(codes + wbase, kWords * 4), f[0], f[1], wi.lane, nwords - wbase);
   }
 }
 
 // ---------------------------------------------------------------- backward
-// The values of two consecutive elements come from one 8-byte LDS read: the
-// pair table holds (v[c0], v[c1]) at index c0 | c1 << BITS, which is exactly
-// the 2*BITS-bit slice of the lane field holding the two codes.
+// The K values of the table live in one register of each wave, lane i
+// holding v[i mod K] (K <= 16 divides 64), and an element's value is read
+// from the lane its code names with one cross-lane permute (ds_bpermute).
+// No LDS array is filled and no barrier is taken, so a wave issues its
+// stream loads as soon as it starts: the backward runs as a grid of
+// one-wave workgroups, one tile each, and the hardware dispatcher streams
+// them through the device.
 template <int BITS>
-__device__ inline f32x2_t pair_values(const f32x2_t* pairs, uint32_t F, int pair) {
-  return pairs[(F >> (2 * BITS * pair)) & ((1u << (2 * BITS)) - 1u)];
-}
-
-template <int DT, int BITS>
-struct Grad {
-  static constexpr int kVecs = 1;   // 16-byte vectors per lane per tile
-  __device__ static void apply(const u32x4_t (&g)[1], uint32_t F, const f32x2_t* pairs,
-                               u32x4_t (&out)[1]) {
-    using H = Half<DT>;
+struct Values {
+  int lane_value;
+  __device__ explicit Values(const TableArgs& tab, int lane) {
+    // v[lane mod K] by a chain of selects over scalar registers.  The values
+    // pass an empty asm barrier first, which keeps them in scalar registers:
+    // otherwise the compiler folds the chain into a per-lane load from the
+    // kernel-argument block, a vector memory load whose wait would hold back
+    // the stream loads.
+    float v = 0.0f;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t w = g[0][k];
-      const f32x2_t v = pair_values<BITS>(pairs, F, k);
-      out[0][k] = H::pack(H::lo(w) * v.x, H::hi(w) * v.y);   // fp32 products, then RNE
+    for (int c = 0; c < (1 << BITS); ++c) {
+      float t = tab.v[c];
+      asm("" : "+s"(t));
+      v = ((lane & ((1 << BITS) - 1)) == c) ? t : v;
     }
+    lane_value = __float_as_int(v);
+  }
+  // v[c] for the code c of this lane; all 64 lanes must take part
+  __device__ float operator()(uint32_t c) const {
+    return __int_as_float(__builtin_amdgcn_ds_bpermute(static_cast<int>(c << 2), lane_value));
   }
 };
 
 template <int DT, int BITS>
-__global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
-    const void* g, const uint32_t* __restrict__ codes, void* gin, int64_t n, int64_t nwords,
-    TableArgs tab) {
-  static_assert(DT != FEWBIT_F32, "fp32 uses bwd32_kernel");
-  constexpr int U = FEWBIT_BWD_UNROLL;
-  constexpr int V = Grad<DT, BITS>::kVecs;
-  constexpr int kWords = 16 * BITS;
-  constexpr int kEsz = (DT == FEWBIT_F32) ? 4 : 2;
+__device__ inline u32x4_t grad16_tile(u32x4_t g, uint32_t F, const Values<BITS>& val) {
+  using H = Half<DT>;
   constexpr uint32_t kMask = (1u << BITS) - 1u;
-  constexpr int kPairs = 1 << (2 * BITS);
-  __shared__ f32x2_t pairs[kPairs];
-  for (int i = threadIdx.x; i < kPairs; i += blockDim.x)
-    pairs[i] = (f32x2_t){tab.v[i & kMask], tab.v[i >> BITS]};
-  __syncthreads();
-  const float* val = reinterpret_cast<const float*>(pairs);   // val[2c] = v[c] (c < K)
+  u32x4_t out;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float v0 = val((F >> (2 * k * BITS)) & kMask);
+    const float v1 = val((F >> ((2 * k + 1) * BITS)) & kMask);
+    out[k] = H::pack(H::lo(g[k]) * v0, H::hi(g[k]) * v1);   // fp32 products, then RNE
+  }
+  return out;
+}
 
-  const WaveIndex wi = wave_index();
+template <int DT, int BITS>
+__global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
+    const uint16_t* g, const uint32_t* __restrict__ codes, uint16_t* gin, int64_t n,
+    int64_t nwords, TableArgs tab) {
+  constexpr int U = FEWBIT_BWD_UNROLL;
+  constexpr int kWords = 16 * BITS;
+  constexpr uint32_t kMask = (1u << BITS) - 1u;
+  const WaveIndex wi = wave_index<FEWBIT_BWD_THREADS>();
+  const Values<BITS> val(tab, wi.lane);
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
-  const char* gb = static_cast<const char*>(g);
-  char* ob = static_cast<char*>(gin);
+  const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
 
   for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
     const int64_t t0 = gi * U;
-    u32x4_t in[U][V], out[U][V];
+    u32x4_t in[U];
     uint32_t F[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const char* p = gb + ((t0 + u) * kTile + lane_off) * kEsz;
-#pragma unroll
-      for (int v = 0; v < V; ++v) in[u][v] = ld_stream(p + 16 * v);
-      F[u] = load_field_full<BITS>(codes + (t0 + u) * kWords, wi.lane);
+      in[u] = Span(g + (t0 + u) * kTile, kSpanBytes).ld16(lane_b);
+      F[u] = load_field_full<BITS>(Span(codes + (t0 + u) * kWords, kWords * 4), wi.lane);
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) Grad<DT, BITS>::apply(in[u], F[u], pairs, out[u]);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      char* q = ob + ((t0 + u) * kTile + lane_off) * kEsz;
-#pragma unroll
-      for (int v = 0; v < V; ++v) st_stream(q + 16 * v, out[u][v]);
-    }
+    for (int u = 0; u < U; ++u)
+      Span(gin + (t0 + u) * kTile, kSpanBytes).st16(lane_b, grad16_tile<DT, BITS>(in[u], F[u], val));
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
-    u32x4_t in[V], out[V];
-    const char* p = gb + (t * kTile + lane_off) * kEsz;
-#pragma unroll
-    for (int v = 0; v < V; ++v) in[v] = ld_stream(p + 16 * v);
-    const uint32_t F = load_field_full<BITS>(codes + t * kWords, wi.lane);
-    Grad<DT, BITS>::apply(in, F, pairs, out);
-    char* q = ob + (t * kTile + lane_off) * kEsz;
-#pragma unroll
-    for (int v = 0; v < V; ++v) st_stream(q + 16 * v, out[v]);
+    const u32x4_t in = Span(g + t * kTile, kSpanBytes).ld16(lane_b);
+    const uint32_t F = load_field_full<BITS>(Span(codes + t * kWords, kWords * 4), wi.lane);
+    Span(gin + t * kTile, kSpanBytes).st16(lane_b, grad16_tile<DT, BITS>(in, F, val));
   }
+  // the partial tile at the end, if any, goes to the wave that would own it
   if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
     const int64_t t = full;
     const int64_t wbase = t * kWords;
-    const uint32_t F = load_field<BITS>(codes + wbase, wi.lane, nwords - wbase);
+    const uint32_t F = load_field<BITS>(Span(codes + wbase, kWords * 4), wi.lane, nwords - wbase);
+    float v[kPerLane];
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) v[j] = val((F >> (BITS * j)) & kMask);   // all lanes
 #pragma unroll
     for (int j = 0; j < kPerLane; ++j) {
       const int64_t e = t * kTile + lane_off + j;
-      if (e < n)
-        Scalar<DT>::store(gin, e, Scalar<DT>::load(g, e) * val[2 * ((F >> (BITS * j)) & kMask)]);
+      if (e < n) Scalar<DT>::store(gin, e, Scalar<DT>::load(g, e) * v[j]);
     }
   }
 }
 
 // fp32 backward on the fp32 tile layout (see fp32 tiles above).
 template <int BITS>
-__device__ inline u32x4_t grad32_half(u32x4_t g, uint32_t f, const f32x2_t* pairs) {
+__device__ inline u32x4_t grad32_half(u32x4_t g, uint32_t f, const Values<BITS>& val) {
+  constexpr uint32_t kMask = (1u << BITS) - 1u;
   u32x4_t out;
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const f32x2_t v = pair_values<BITS>(pairs, f, k);
-    out[2 * k] = __float_as_uint(__uint_as_float(g[2 * k]) * v.x);
-    out[2 * k + 1] = __float_as_uint(__uint_as_float(g[2 * k + 1]) * v.y);
-  }
+  for (int j = 0; j < 4; ++j)
+    out[j] = __float_as_uint(__uint_as_float(g[j]) * val((f >> (BITS * j)) & kMask));
   return out;
 }
 
@@ -958,17 +989,12 @@ __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd32_kernel(
   constexpr int U = FEWBIT_BWD32_UNROLL;
   constexpr int kWords = Codes32<BITS>::kWords;
   constexpr uint32_t kMask = (1u << BITS) - 1u;
-  constexpr int kPairs = 1 << (2 * BITS);
-  __shared__ f32x2_t pairs[kPairs];
-  for (int i = threadIdx.x; i < kPairs; i += blockDim.x)
-    pairs[i] = (f32x2_t){tab.v[i & kMask], tab.v[i >> BITS]};
-  __syncthreads();
-  const float* val = reinterpret_cast<const float*>(pairs);   // val[2c] = v[c] (c < K)
-
-  const WaveIndex wi = wave_index();
+  const WaveIndex wi = wave_index<FEWBIT_BWD_THREADS>();
+  const Values<BITS> val(tab, wi.lane);
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * 4;
+  const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
 
   for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
     const int64_t t0 = gi * U;
@@ -978,21 +1004,21 @@ __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd32_kernel(
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        in[u][h] = ld_stream(g + (t0 + u) * kTile + h * 256 + lane_off);
-        f[u][h] = load_field32<BITS, true>(codes + (t0 + u) * kWords, h, wi.lane, kWords);
+        in[u][h] = Span(g + (t0 + u) * kTile + h * 256, kSpanBytes).ld16(lane_b);
+        f[u][h] = load_field32<BITS, true>(Span(codes + (t0 + u) * kWords, kWords * 4), h, wi.lane, kWords);
       }
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
-        st_stream(gin + (t0 + u) * kTile + h * 256 + lane_off, grad32_half<BITS>(in[u][h], f[u][h], pairs));
+        Span(gin + (t0 + u) * kTile + h * 256, kSpanBytes).st16(lane_b, grad32_half<BITS>(in[u][h], f[u][h], val));
   }
   for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const u32x4_t in = ld_stream(g + t * kTile + h * 256 + lane_off);
-      const uint32_t f = load_field32<BITS, true>(codes + t * kWords, h, wi.lane, kWords);
-      st_stream(gin + t * kTile + h * 256 + lane_off, grad32_half<BITS>(in, f, pairs));
+      const u32x4_t in = Span(g + t * kTile + h * 256, kSpanBytes).ld16(lane_b);
+      const uint32_t f = load_field32<BITS, true>(Span(codes + t * kWords, kWords * 4), h, wi.lane, kWords);
+      Span(gin + t * kTile + h * 256, kSpanBytes).st16(lane_b, grad32_half<BITS>(in, f, val));
     }
   }
   if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
@@ -1000,11 +1026,14 @@ __global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd32_kernel(
     const int64_t wbase = t * kWords;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const uint32_t f = load_field32<BITS, false>(codes + wbase, h, wi.lane, nwords - wbase);
+      const uint32_t f = load_field32<BITS, false>(Span(codes + wbase, kWords * 4), h, wi.lane, nwords - wbase);
+      float v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = val((f >> (BITS * j)) & kMask);   // all lanes
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int64_t e = t * kTile + h * 256 + lane_off + j;
-        if (e < n) gin[e] = g[e] * val[2 * ((f >> (BITS * j)) & kMask)];
+        if (e < n) gin[e] = g[e] * v[j];
       }
     }
   }
@@ -1055,13 +1084,17 @@ int device_cus() {
   return c;
 }
 
-// Workgroups for n elements when each has `waves_per_block` streaming waves:
-// one tile per wave at most, capped at wg_per_cu per compute unit.
-dim3 grid_for(int64_t n, int waves_per_block, int wg_per_cu) {
+// Workgroups for n elements when each has `waves_per_block` streaming waves
+// that take `unroll` tiles per loop trip: one tile group per wave at most,
+// capped at wg_per_cu per compute unit when wg_per_cu > 0.
+dim3 grid_for(int64_t n, int waves_per_block, int wg_per_cu, int unroll) {
   const int64_t tiles = (n + kTile - 1) / kTile;
-  int64_t blocks = (tiles + waves_per_block - 1) / waves_per_block;
-  const int64_t cap = static_cast<int64_t>(device_cus()) * wg_per_cu;
-  if (blocks > cap) blocks = cap;
+  const int64_t groups = (tiles + unroll - 1) / unroll;
+  int64_t blocks = (groups + waves_per_block - 1) / waves_per_block;
+  if (wg_per_cu > 0) {
+    const int64_t cap = static_cast<int64_t>(device_cus()) * wg_per_cu;
+    if (blocks > cap) blocks = cap;
+  }
   if (blocks < 1) blocks = 1;
   return dim3(static_cast<unsigned>(blocks));
 }
@@ -1121,13 +1154,13 @@ void launch_fwd(const Launch& L) {
   const int64_t nw = (L.n * BITS + 31) / 32;
   const int sym = (L.t->flags & FEWBIT_FLAG_SYMMETRIC) ? 1 : 0;
   if constexpr (DT == FEWBIT_F32) {
-    const dim3 grid = grid_for(L.n, FEWBIT_FWD32_THREADS / kWave, FEWBIT_FWD32_WG_PER_CU);
+    const dim3 grid = grid_for(L.n, FEWBIT_FWD32_THREADS / kWave, FEWBIT_FWD32_WG_PER_CU, FEWBIT_FWD32_UNROLL);
     (void)hipGetLastError();
     hipLaunchKernelGGL((fwd32_kernel<BITS, ACT>), grid, dim3(FEWBIT_FWD32_THREADS), 0, L.s,
                        static_cast<const float*>(L.in), static_cast<float*>(L.out), L.codes, L.n,
                        nw, table_args(L.t), sym);
   } else {
-    const dim3 grid = grid_for(L.n, FEWBIT_FWD16_STREAM_WAVES, FEWBIT_FWD16_WG_PER_CU);
+    const dim3 grid = grid_for(L.n, FEWBIT_FWD16_STREAM_WAVES, FEWBIT_FWD16_WG_PER_CU, FEWBIT_FWD16_UNROLL);
     (void)hipGetLastError();
     hipLaunchKernelGGL((fwd16_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16_THREADS), 0, L.s,
                        static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
@@ -1161,15 +1194,17 @@ void launch_fwd_bits(const Launch& L) {
 template <int DT, int BITS>
 void launch_bwd(const Launch& L) {
   const int64_t nw = (L.n * BITS + 31) / 32;
-  const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS / kWave, FEWBIT_BWD_WG_PER_CU);
+  const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS / kWave, FEWBIT_BWD_WG_PER_CU,
+                            DT == FEWBIT_F32 ? FEWBIT_BWD32_UNROLL : FEWBIT_BWD_UNROLL);
   (void)hipGetLastError();
   if constexpr (DT == FEWBIT_F32)
     hipLaunchKernelGGL((bwd32_kernel<BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s,
                        static_cast<const float*>(L.in), L.codes, static_cast<float*>(L.out), L.n,
                        nw, table_args(L.t));
   else
-    hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s, L.in,
-                       L.codes, L.out, L.n, nw, table_args(L.t));
+    hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s,
+                       static_cast<const uint16_t*>(L.in), L.codes, static_cast<uint16_t*>(L.out),
+                       L.n, nw, table_args(L.t));
 }
 
 template <int DT>
