@@ -168,6 +168,13 @@ int64_t fewbit_packed_words(int64_t n, int32_t bits);
 int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, void* y,
                uint32_t* codes, int64_t n, void* stream);
 
+/* Element count from which an fp16 / bf16 forward runs the table kernel
+ * (outputs and indices looked up per input bit pattern); smaller forwards
+ * evaluate f and the compares per element.  Both give the same results;
+ * this only tells a caller (or a test) which kernel a given n reaches.
+ * Host only, no device access. */
+int64_t fewbit_fwd16_table_min(void);
+
 /*
  * fewbit_bwd -- backward of the few-bit activation (Eq. (1) with f'(x)
  * replaced by q(x); Listing 1, backward).

@@ -7,12 +7,13 @@ include/fewbit.h); this package is its Python binding.
 """
 from ._lib import (ACTS, BF16, DTYPES, F16, F32, FLAG_REFINE, FLAG_SYMMETRIC, GELU, LIB_PATH, RELU, SELU,
                    SIGMOID, SILU, SOFTPLUS, TANH, W_MIXTURE, W_NORMAL, W_UNIFORM, FewbitError,
-                   Table, Weight, bwd, bwd_raw, fit_table, fwd, fwd_raw, packed_words, strerror)
+                   Table, Weight, bwd, bwd_raw, fit_table, fwd, fwd16_table_min, fwd_raw, packed_words,
+                   strerror)
 from .autograd import FewBitActivation, FewBitAct
 
 __all__ = [
     "ACTS", "BF16", "DTYPES", "F16", "F32", "FLAG_REFINE", "FLAG_SYMMETRIC", "GELU", "LIB_PATH", "RELU", "SELU",
     "SIGMOID", "SILU", "SOFTPLUS", "TANH", "W_MIXTURE", "W_NORMAL", "W_UNIFORM", "FewbitError", "Table", "Weight",
-    "bwd", "bwd_raw", "fit_table", "fwd", "fwd_raw", "packed_words", "strerror",
+    "bwd", "bwd_raw", "fit_table", "fwd", "fwd16_table_min", "fwd_raw", "packed_words", "strerror",
     "FewBitActivation", "FewBitAct",
 ]

@@ -68,6 +68,8 @@ def _load():
     L.fewbit_fwd.argtypes = [C.POINTER(CTable), i32, vp, vp, vp, i64, vp]
     L.fewbit_bwd.restype = C.c_int
     L.fewbit_bwd.argtypes = [C.POINTER(CTable), i32, vp, vp, vp, i64, vp]
+    L.fewbit_fwd16_table_min.restype = i64
+    L.fewbit_fwd16_table_min.argtypes = []
     L.fewbit_strerror.restype = C.c_char_p
     L.fewbit_strerror.argtypes = [i32]
     return L
@@ -163,6 +165,11 @@ def fit_table(act, bits: int, weight: Weight, n_grid: int, symmetric: bool = Fal
 
 def packed_words(n: int, bits: int) -> int:
     return int(lib.fewbit_packed_words(int(n), int(bits)))
+
+
+def fwd16_table_min() -> int:
+    """Element count from which fp16 / bf16 forwards use the table kernel."""
+    return int(lib.fewbit_fwd16_table_min())
 
 
 # ---------------------------------------------------------------- raw pointers

@@ -68,6 +68,14 @@
 #ifndef FEWBIT_FWD16_STREAM_WAVES
 #define FEWBIT_FWD16_STREAM_WAVES (FEWBIT_FWD16_THREADS / 64)
 #endif
+// the fp16 / bf16 forward by evaluation (no tables): threads per workgroup,
+// and the element count from which the table kernel is used instead
+#ifndef FEWBIT_FWD16V_THREADS
+#define FEWBIT_FWD16V_THREADS 64
+#endif
+#ifndef FEWBIT_FWD16_TABLE_MIN
+#define FEWBIT_FWD16_TABLE_MIN (int64_t{1} << 22)
+#endif
 #ifndef FEWBIT_FWD32_THREADS
 #define FEWBIT_FWD32_THREADS 256
 #endif
@@ -85,6 +93,9 @@
 #endif
 #ifndef FEWBIT_BWD_UNROLL
 #define FEWBIT_BWD_UNROLL 1
+#endif
+#ifndef FEWBIT_BWD32_THREADS
+#define FEWBIT_BWD32_THREADS 256
 #endif
 #ifndef FEWBIT_BWD32_UNROLL
 #define FEWBIT_BWD32_UNROLL 1
@@ -745,6 +756,60 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   }
 }
 
+// fp16 / bf16 forward by evaluation: f and the compares for every element,
+// no tables.  The table kernel above needs ~3 us of setup per launch and a
+// persistent grid; below FEWBIT_FWD16_TABLE_MIN elements this kernel, one
+// wave per tile with no setup, is faster.  Outputs are the table kernel's:
+// the tables hold this same f and rounding.
+// y and the two codes of the element pair in word w; the codes go to bits
+// shift .. shift + 2*BITS - 1 of F.
+template <int DT, int BITS, int ACT>
+__device__ inline uint32_t fwd16v_pair(uint32_t w, const Bounds& bd, int symmetric, uint32_t& F,
+                                       int shift) {
+  using H = Half<DT>;
+  const float a = H::lo(w), b = H::hi(w);
+  F |= (classify<BITS>(symmetric ? fabsf(a) : a, bd) << shift) |
+       (classify<BITS>(symmetric ? fabsf(b) : b, bd) << (shift + BITS));
+  return H::pack(Act<DT, ACT>::f(a), Act<DT, ACT>::f(b));
+}
+
+template <int DT, int BITS, int ACT>
+__global__ __launch_bounds__(FEWBIT_FWD16V_THREADS) void fwd16v_kernel(
+    const uint16_t* x, uint16_t* y, uint32_t* __restrict__ codes, int64_t n, int64_t nwords,
+    TableArgs tab, int symmetric) {
+  constexpr int kWords = 16 * BITS;
+  const Bounds bd = bounds_of(tab);
+  const WaveIndex wi = wave_index<FEWBIT_FWD16V_THREADS>();
+  const int64_t full = n / kTile;
+  const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
+  const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
+  for (int64_t t = wi.wave; t < full; t += wi.nwaves) {
+    const u32x4_t in = Span(x + t * kTile, kSpanBytes).ld16(lane_b);
+    u32x4_t out;
+    uint32_t F = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) out[k] = fwd16v_pair<DT, BITS, ACT>(in[k], bd, symmetric, F, 2 * k * BITS);
+    Span(y + t * kTile, kSpanBytes).st16(lane_b, out);
+    pack_store_full<BITS>(Span(codes + t * kWords, kWords * 4), F, wi.lane);
+  }
+  // the partial tile at the end, if any, goes to the wave that would own it
+  if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
+    const int64_t t = full;
+    uint32_t F = 0;
+#pragma unroll
+    for (int j = 0; j < kPerLane; ++j) {
+      const int64_t e = t * kTile + lane_off + j;
+      if (e < n) {
+        const float v = Half<DT>::widen(x[e]);
+        y[e] = static_cast<uint16_t>(Half<DT>::pack(Act<DT, ACT>::f(v), 0.0f) & 0xFFFFu);
+        F |= classify<BITS>(symmetric ? fabsf(v) : v, bd) << (BITS * j);
+      }
+    }
+    const int64_t wbase = t * kWords;
+    pack_store<BITS>(Span(codes + wbase, kWords * 4), F, wi.lane, nwords - wbase);
+  }
+}
+
 // ---------------------------------------------------------------- fp32 tiles
 // An fp32 tile is 512 elements in two halves of 256; lane l holds elements
 // 4l .. 4l+3 of each half, so each 16-byte access instruction covers 1 KiB
@@ -983,13 +1048,13 @@ __device__ inline u32x4_t grad32_half(u32x4_t g, uint32_t f, const Values<BITS>&
 }
 
 template <int BITS>
-__global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd32_kernel(
+__global__ __launch_bounds__(FEWBIT_BWD32_THREADS) void bwd32_kernel(
     const float* g, const uint32_t* __restrict__ codes, float* gin, int64_t n, int64_t nwords,
     TableArgs tab) {
   constexpr int U = FEWBIT_BWD32_UNROLL;
   constexpr int kWords = Codes32<BITS>::kWords;
   constexpr uint32_t kMask = (1u << BITS) - 1u;
-  const WaveIndex wi = wave_index<FEWBIT_BWD_THREADS>();
+  const WaveIndex wi = wave_index<FEWBIT_BWD32_THREADS>();
   const Values<BITS> val(tab, wi.lane);
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
@@ -1159,6 +1224,12 @@ void launch_fwd(const Launch& L) {
     hipLaunchKernelGGL((fwd32_kernel<BITS, ACT>), grid, dim3(FEWBIT_FWD32_THREADS), 0, L.s,
                        static_cast<const float*>(L.in), static_cast<float*>(L.out), L.codes, L.n,
                        nw, table_args(L.t), sym);
+  } else if (L.n < FEWBIT_FWD16_TABLE_MIN) {
+    const dim3 grid = grid_for(L.n, FEWBIT_FWD16V_THREADS / kWave, 0, 1);
+    (void)hipGetLastError();
+    hipLaunchKernelGGL((fwd16v_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16V_THREADS), 0, L.s,
+                       static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
+                       L.n, nw, table_args(L.t), sym);
   } else {
     const dim3 grid = grid_for(L.n, FEWBIT_FWD16_STREAM_WAVES, FEWBIT_FWD16_WG_PER_CU, FEWBIT_FWD16_UNROLL);
     (void)hipGetLastError();
@@ -1194,17 +1265,18 @@ void launch_fwd_bits(const Launch& L) {
 template <int DT, int BITS>
 void launch_bwd(const Launch& L) {
   const int64_t nw = (L.n * BITS + 31) / 32;
-  const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS / kWave, FEWBIT_BWD_WG_PER_CU,
-                            DT == FEWBIT_F32 ? FEWBIT_BWD32_UNROLL : FEWBIT_BWD_UNROLL);
   (void)hipGetLastError();
-  if constexpr (DT == FEWBIT_F32)
-    hipLaunchKernelGGL((bwd32_kernel<BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s,
+  if constexpr (DT == FEWBIT_F32) {
+    const dim3 grid = grid_for(L.n, FEWBIT_BWD32_THREADS / kWave, FEWBIT_BWD_WG_PER_CU, FEWBIT_BWD32_UNROLL);
+    hipLaunchKernelGGL((bwd32_kernel<BITS>), grid, dim3(FEWBIT_BWD32_THREADS), 0, L.s,
                        static_cast<const float*>(L.in), L.codes, static_cast<float*>(L.out), L.n,
                        nw, table_args(L.t));
-  else
+  } else {
+    const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS / kWave, FEWBIT_BWD_WG_PER_CU, FEWBIT_BWD_UNROLL);
     hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s,
                        static_cast<const uint16_t*>(L.in), L.codes, static_cast<uint16_t*>(L.out),
                        L.n, nw, table_args(L.t));
+  }
 }
 
 template <int DT>
@@ -1242,7 +1314,7 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   if (misaligned(x) || misaligned(y) || misaligned(codes)) return FEWBIT_E_ALIGN;
   rc = check_stream_device(static_cast<hipStream_t>(stream));
   if (rc != FEWBIT_OK) return rc;
-  if (dtype != FEWBIT_F32) {
+  if (dtype != FEWBIT_F32 && n >= FEWBIT_FWD16_TABLE_MIN) {
     rc = ensure_output_tables();
     if (rc != FEWBIT_OK) return rc;
   }
@@ -1254,6 +1326,8 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   }
   return launch_status("fewbit_fwd");
 }
+
+extern "C" int64_t fewbit_fwd16_table_min(void) { return FEWBIT_FWD16_TABLE_MIN; }
 
 extern "C" int fewbit_bwd(const fewbit_table* t, int32_t dtype, const void* grad_out,
                           const uint32_t* codes, void* grad_in, int64_t n, void* stream) {

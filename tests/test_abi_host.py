@@ -33,10 +33,16 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     names = declared_functions()
     assert set(names) == {"fewbit_fit_table", "fewbit_packed_words", "fewbit_fwd",
-                          "fewbit_bwd", "fewbit_strerror"}
+                          "fewbit_fwd16_table_min", "fewbit_bwd", "fewbit_strerror"}
     raw = C.CDLL(P.LIB_PATH)
     for name in names:
         assert hasattr(raw, name), name
+
+
+def test_fwd16_table_min():
+    # a positive element count, a whole number of 512-element tiles
+    m = P.fwd16_table_min()
+    assert m > 0 and m % 512 == 0
 
 
 def test_packed_words():

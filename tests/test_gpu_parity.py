@@ -5,6 +5,8 @@ or 1 ulp (fp16 / bf16).  Cases: all five workloads at full size (the sizes
 the benchmark runs, in its launch configuration), the same workloads cut to
 ragged lengths, an edge-size sweep over every dtype x bits x activation,
 special values, boundaries, ReLU / SELU / Softplus (Table 1's other rows),
+both fp16 / bf16 forward kernels (per-element evaluation below
+fwd16_table_min() elements, table lookups from there on),
 the symmetric (|x|) tables of Sigmoid and Tanh,
 in-place aliasing, a second stream, canaries past every output, and the
 autograd wrapper.
@@ -166,6 +168,28 @@ def test_special_values_and_boundaries(act, dt):
     _run_synthetic(act, bits, dt, x, g, f"special {act}")
 
 
+# fp16 / bf16 forwards from fwd16_table_min() elements on run the table
+# kernel (LDS lookups per input bit pattern); smaller ones evaluate f and
+# the compares per element.  The cases above are mostly small; this one
+# takes every activation, half type and bit width through the table kernel,
+# with the special values and boundary neighbours in the mix.
+@pytest.mark.parametrize("act", ["gelu", "silu", "sigmoid", "tanh"] + MORE_ACTS)
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+def test_table_kernel_every_activation(act, dt):
+    n = P.fwd16_table_min() + 1234
+    rng = np.random.default_rng(17)
+    for bits in (1, 2, 3, 4):
+        s, v, table = _synthetic_table(act, bits)
+        special = O.round_array(ODT[dt], _special_values(dt, s))
+        hb = O.round_array(ODT[dt], s.astype(np.float64))
+        special = np.concatenate([special, hb, (hb + 1).astype(np.uint16), (hb - 1).astype(np.uint16)])
+        x = O.round_array(ODT[dt], rng.uniform(-20, 20, n))
+        pos = rng.choice(n, special.size * 64, replace=False)
+        x[pos] = np.tile(special, 64)
+        g = O.round_array(ODT[dt], rng.normal(0, 1, n))
+        _run_synthetic(act, bits, dt, x, g, f"table kernel {act}")
+
+
 # Symmetric tables (Fig. 3 caption: an even f' is fitted on [0, B] and the
 # bins apply to |x|), fitted by the oracle for the Sigmoid and Tanh inputs.
 SYM = sorted((k.split("/")[0], int(k.split("/")[1][1:])) for k in TABLES if k.endswith("/sym"))
@@ -183,7 +207,7 @@ def test_symmetric_full_size(name, bits):
 @pytest.mark.parametrize("name,bits", SYM, ids=[f"{n}-b{b}" for n, b in SYM])
 def test_symmetric_half_types(name, bits, dt):
     w = WL.WORKLOADS[name]
-    for n in (1, 513, 4097, (1 << 20) + 3):
+    for n in (1, 513, 4097, (1 << 20) + 3, P.fwd16_table_min() + 3):
         x = WL.draw(w.x_dist, w.x_scale, n, dt, w.seed)
         g = WL.draw("normal", w.g_sigma, n, dt, w.seed + 1000)
         run_case(f"{name}/b{bits}/sym", dt, x, g, label=f"{name} b{bits} sym {dt} n={n}")
