@@ -41,6 +41,17 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def kernel_name(kind: str, dtype: str, bits: int, act: str, n: int, table_min: int) -> str:
+    """Name of the library kernel a pass runs, as the rocprofv3 summaries
+    print it."""
+    if kind == "bwd":
+        return f"bwd32_kernel<f32,{bits}>" if dtype == "f32" else f"bwd_kernel<{dtype},{bits}>"
+    if dtype == "f32":
+        return f"fwd32_kernel<f32,{bits},{act}>"
+    k = "fwd16_kernel" if n >= table_min else "fwd16v_kernel"
+    return f"{k}<{dtype},{bits},{act}>"
+
+
 def measured_traffic(workload: str, bits: int, kernel: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if
     it was taken on the current kernel source; else None."""
@@ -65,13 +76,13 @@ def _kernel_key(name: str):
     """'fwd16_kernel<bf16,3,gelu>' style key of a library kernel named in a
     rocprofv3 csv, or the plain name for any other kernel."""
     import re
-    m = re.search(r"(fwd16_kernel|fwd32_kernel|bwd32_kernel|bwd_kernel)<([0-9, ]+)>", name)
+    m = re.search(r"(fwd16v_kernel|fwd16_kernel|fwd32_kernel|bwd32_kernel|bwd_kernel)<([0-9, ]+)>", name)
     if not m:
         base = name.replace("(anonymous namespace)::", "").replace("void ", "")
         return base.split("(")[0].strip() or name
     args = [int(a) for a in m.group(2).split(",")]
-    if m.group(1) == "fwd16_kernel":
-        return f"fwd16_kernel<{DT_NAMES[args[0]]},{args[1]},{ACT_NAMES[args[2]]}>"
+    if m.group(1) in ("fwd16_kernel", "fwd16v_kernel"):
+        return f"{m.group(1)}<{DT_NAMES[args[0]]},{args[1]},{ACT_NAMES[args[2]]}>"
     if m.group(1) == "fwd32_kernel":
         return f"fwd32_kernel<f32,{args[0]},{ACT_NAMES[args[1]]}>"
     if m.group(1) == "bwd32_kernel":
@@ -152,12 +163,23 @@ def summarize_rocprof(trace_dir, fetch_dir, write_dir, workload, bits, out_traff
             kind = "fwd" if key.startswith("fwd") else "bwd"
             traffic[f"{workload}/b{bits}/{kind}"] = {
                 "kernel": key, "fetch_bytes": round(fb), "write_bytes": round(wb),
-                "hbm_bytes": round(fb + wb), "algorithmic_bytes": alg}
+                "hbm_bytes": round(fb + wb), "algorithmic_bytes": alg,
+                "calibration": {"kernel": copy[0], "bytes_each_way": copy_bytes,
+                                "fetch_factor": f_fetch, "write_factor": f_write}}
         if out_traffic:
+            # keep the other workloads' entries taken on the same kernel source
+            path = os.path.join(ROOT, "profiles", "traffic.json")
+            launches = {}
+            try:
+                with open(path) as fh:
+                    old = json.load(fh)
+                if old.get("kernel_source_hash") == kernel_source_hash():
+                    launches = old.get("launches", {})
+            except (OSError, ValueError):
+                pass
+            launches.update(traffic)
             rec = {"kernel_source_hash": kernel_source_hash(),
-                   "calibration": {"kernel": copy[0], "bytes_each_way": copy_bytes,
-                                   "fetch_factor": f_fetch, "write_factor": f_write},
-                   "launches": traffic}
+                   "launches": dict(sorted(launches.items()))}
             with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as fh:
                 json.dump(rec, fh, indent=1)
                 fh.write("\n")
@@ -366,8 +388,7 @@ def main():
         "copy_ceiling": {"GB/s": round(copy_gbps, 2), "ms": round(copy_ms, 5),
                          "what": "torch copy_ of x (read+write, same element count)"},
         "roofline": {
-            "kernel": (f"fwd{32 if w.dtype == 'f32' else 16}_kernel" if dom == "fwd" else "bwd_kernel")
-                      + f"<{w.dtype},{bits},{w.act}>",
+            "kernel": kernel_name(dom, w.dtype, bits, w.act, n, P.fwd16_table_min()),
             "bound": "hbm",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBPS,

@@ -25,10 +25,11 @@
  *     the launch grid) and, for the fp16 / bf16 forward, static device
  *     tables of f over all 65536 input patterns of each activation and
  *     type (1.75 MiB of module memory).  The first fp16 / bf16 fewbit_fwd on
- *     a device evaluates those tables on a private non-blocking stream and
- *     waits for that stream alone; it therefore must not be made while a
- *     stream is being captured into a graph in a mode that forbids
- *     synchronisation.  Calls are reentrant and thread-safe.
+ *     a device with n >= fewbit_fwd16_table_min() evaluates those tables on
+ *     a private non-blocking stream and waits for that stream alone; it
+ *     therefore must not be made while a stream is being captured into a
+ *     graph in a mode that forbids synchronisation.  Calls are reentrant
+ *     and thread-safe.
  *   - No C++ exception crosses this interface.
  */
 #ifndef FEWBIT_H
