@@ -445,6 +445,46 @@ __device__ inline uint32_t classify(float x, const Bounds& bd) {
   return idx;
 }
 
+// The classification of the per-element kernels.  Up to 3 bits it is the
+// select tree above.  At 4 bits the tree's last level alone takes 7 selects,
+// so there the boundaries are spread over the lanes of one register (lane i
+// holds s[i], i < 15): the first level compares with the middle boundary,
+// held in a scalar register, and each later level reads its boundary from
+// the lane the search has reached with one cross-lane permute (ds_bpermute),
+// ~3 VALU operations and one permute per level.  All 64 lanes must take part
+// in every call (the permutes read other lanes).
+template <int BITS>
+struct Search {
+  static constexpr uint32_t K = 1u << BITS;
+  static constexpr bool kPermute = BITS == 4;
+  Bounds bd;          // the select tree's boundaries (BITS <= 3)
+  float mid;          // s[K/2 - 1]
+  int lane_bound;     // s[lane] for lane < 15
+  __device__ Search(const TableArgs& tab, int lane) : bd(bounds_of(tab)) {
+    float v = 0.0f;
+#pragma unroll
+    for (int m = 0; m < 15; ++m) {
+      v = (lane == m) ? bd.s[m] : v;
+      if (m == static_cast<int>(K / 2 - 1)) mid = bd.s[m];
+    }
+    lane_bound = __float_as_int(v);
+  }
+  __device__ uint32_t operator()(float x) const {
+    if constexpr (!kPermute) {
+      return classify<BITS>(x, bd);
+    } else {
+      uint32_t idx = x >= mid ? K / 2 : 0u;
+#pragma unroll
+      for (uint32_t step = K / 4; step >= 1; step /= 2) {
+        const float b = __int_as_float(
+            __builtin_amdgcn_ds_bpermute(static_cast<int>((idx + step - 1) << 2), lane_bound));
+        idx += x >= b ? step : 0u;
+      }
+      return idx;
+    }
+  }
+};
+
 // ---------------------------------------------------------------- packing
 // quad_perm DPP control: lane k of each quad reads lane sel[k] of the quad.
 constexpr int quad_perm(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
@@ -764,12 +804,11 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
 // y and the two codes of the element pair in word w; the codes go to bits
 // shift .. shift + 2*BITS - 1 of F.
 template <int DT, int BITS, int ACT>
-__device__ inline uint32_t fwd16v_pair(uint32_t w, const Bounds& bd, int symmetric, uint32_t& F,
+__device__ inline uint32_t fwd16v_pair(uint32_t w, const Search<BITS>& cl, int symmetric, uint32_t& F,
                                        int shift) {
   using H = Half<DT>;
   const float a = H::lo(w), b = H::hi(w);
-  F |= (classify<BITS>(symmetric ? fabsf(a) : a, bd) << shift) |
-       (classify<BITS>(symmetric ? fabsf(b) : b, bd) << (shift + BITS));
+  F |= (cl(symmetric ? fabsf(a) : a) << shift) | (cl(symmetric ? fabsf(b) : b) << (shift + BITS));
   return H::pack(Act<DT, ACT>::f(a), Act<DT, ACT>::f(b));
 }
 
@@ -778,8 +817,8 @@ __global__ __launch_bounds__(FEWBIT_FWD16V_THREADS) void fwd16v_kernel(
     const uint16_t* x, uint16_t* y, uint32_t* __restrict__ codes, int64_t n, int64_t nwords,
     TableArgs tab, int symmetric) {
   constexpr int kWords = 16 * BITS;
-  const Bounds bd = bounds_of(tab);
   const WaveIndex wi = wave_index<FEWBIT_FWD16V_THREADS>();
+  const Search<BITS> cl(tab, wi.lane);
   const int64_t full = n / kTile;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
   const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
@@ -788,7 +827,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16V_THREADS) void fwd16v_kernel(
     u32x4_t out;
     uint32_t F = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) out[k] = fwd16v_pair<DT, BITS, ACT>(in[k], bd, symmetric, F, 2 * k * BITS);
+    for (int k = 0; k < 4; ++k) out[k] = fwd16v_pair<DT, BITS, ACT>(in[k], cl, symmetric, F, 2 * k * BITS);
     Span(y + t * kTile, kSpanBytes).st16(lane_b, out);
     pack_store_full<BITS>(Span(codes + t * kWords, kWords * 4), F, wi.lane);
   }
@@ -799,10 +838,11 @@ __global__ __launch_bounds__(FEWBIT_FWD16V_THREADS) void fwd16v_kernel(
 #pragma unroll
     for (int j = 0; j < kPerLane; ++j) {
       const int64_t e = t * kTile + lane_off + j;
+      const float v = e < n ? Half<DT>::widen(x[e]) : 0.0f;
+      const uint32_t c = cl(symmetric ? fabsf(v) : v);       // all lanes
       if (e < n) {
-        const float v = Half<DT>::widen(x[e]);
         y[e] = static_cast<uint16_t>(Half<DT>::pack(Act<DT, ACT>::f(v), 0.0f) & 0xFFFFu);
-        F |= classify<BITS>(symmetric ? fabsf(v) : v, bd) << (BITS * j);
+        F |= c << (BITS * j);
       }
     }
     const int64_t wbase = t * kWords;
@@ -868,14 +908,14 @@ __device__ inline uint32_t load_field32(const Span& base, int v, int lane, int64
 
 // ---------------------------------------------------------------- forward, fp32
 template <int BITS, int ACT>
-__device__ inline void fwd32_half(u32x4_t in, const Bounds& bd, int symmetric, u32x4_t& out,
+__device__ inline void fwd32_half(u32x4_t in, const Search<BITS>& cl, int symmetric, u32x4_t& out,
                                   uint32_t& f) {
   f = 0;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const float xv = __uint_as_float(in[j]);
     out[j] = __float_as_uint(Act<FEWBIT_F32, ACT>::f(xv));
-    f |= classify<BITS>(symmetric ? fabsf(xv) : xv, bd) << (BITS * j);
+    f |= cl(symmetric ? fabsf(xv) : xv) << (BITS * j);
   }
 }
 
@@ -885,8 +925,8 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
     TableArgs tab, int symmetric) {
   constexpr int U = FEWBIT_FWD32_UNROLL;
   constexpr int kWords = Codes32<BITS>::kWords;
-  const Bounds bd = bounds_of(tab);
   const WaveIndex wi = wave_index<FEWBIT_FWD32_THREADS>();
+  const Search<BITS> cl(tab, wi.lane);
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * 4;
@@ -903,7 +943,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) fwd32_half<BITS, ACT>(in[u][h], bd, symmetric, out[u][h], f[u][h]);
+      for (int h = 0; h < 2; ++h) fwd32_half<BITS, ACT>(in[u][h], cl, symmetric, out[u][h], f[u][h]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
 #pragma unroll
@@ -916,7 +956,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
     uint32_t f[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      fwd32_half<BITS, ACT>(Span(x + t * kTile + h * 256, kSpanBytes).ld16(lane_b), bd, symmetric,
+      fwd32_half<BITS, ACT>(Span(x + t * kTile + h * 256, kSpanBytes).ld16(lane_b), cl, symmetric,
                             out[h], f[h]);
       Span(y + t * kTile + h * 256, kSpanBytes).st16(lane_b, out[h]);
     }
@@ -931,10 +971,11 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int64_t e = t * kTile + h * 256 + lane_off + j;
+        const float xv = e < n ? x[e] : 0.0f;
+        const uint32_t c = cl(symmetric ? fabsf(xv) : xv);  // all lanes
         if (e < n) {
-          const float xv = x[e];
           y[e] = Act<FEWBIT_F32, ACT>::f(xv);
-          f[h] |= classify<BITS>(symmetric ? fabsf(xv) : xv, bd) << (BITS * j);
+          f[h] |= c << (BITS * j);
         }
       }
     const int64_t wbase = t * kWords;
