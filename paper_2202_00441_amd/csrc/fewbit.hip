@@ -19,20 +19,23 @@
 // Each packed word has one value, written by its lane (and by lanes that
 // store an identical copy, so that full tiles need no masking).
 //
-// Streams are read and written with non-temporal 16-byte accesses (nothing
-// is reused), by a grid sized to the device's compute units so each wave
-// walks many tiles.
+// Streams are read and written with non-temporal 16-byte buffer accesses
+// (nothing is reused).  Most kernels run one wave per tile and let the
+// hardware dispatcher balance the compute units; the table-based fp16 /
+// bf16 forward is persistent (see the launch-shape knobs below).
 //
 // fp16 / bf16 forward.  Output pattern and interval index are functions of
-// the 16-bit input pattern alone, so each workgroup looks both up in LDS
-// tables over all 65536 patterns: the outputs (evaluated once per device by
-// a table kernel) and the indices (4 bits per pattern, built per launch from
-// the boundaries).  A lookup costs two LDS reads instead of an evaluation of
-// f and 2^b - 1 compares.  The fp32 forward evaluates f and compares against
-// the boundaries held in scalar registers.
+// the 16-bit input pattern alone, so from FEWBIT_FWD16_TABLE_MIN elements on
+// each workgroup looks both up in LDS tables over all 65536 patterns: the
+// outputs (evaluated once per device by a table kernel) and the indices
+// (4 bits per pattern, built per launch from the boundaries).  A lookup
+// costs two LDS reads instead of an evaluation of f and the compares.
+// Smaller fp16 / bf16 forwards, and every fp32 forward, evaluate f and
+// search the boundaries per element.
 //
 // The fitted table travels as kernel arguments (scalar registers); the
-// backward mirrors its values into LDS for per-lane lookup.
+// backward spreads the values over the lanes of one register and reads
+// them with cross-lane permutes.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
