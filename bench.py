@@ -33,11 +33,37 @@ def algorithmic_bytes(n: int, dtype: str, bits: int) -> float:
     return n * (2 * s + bits / 8.0)
 
 
+def _code_tokens(src: str) -> str:
+    """C/C++ source without comments and with whitespace runs collapsed:
+    an edit of comments or layout does not change the kernels."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash() -> str:
+    """Hash of the kernel source's code (comments and layout ignored)."""
     h = hashlib.sha256()
     for f in ("paper_2202_00441_amd/csrc/fewbit.hip",):
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
+            h.update(_code_tokens(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
