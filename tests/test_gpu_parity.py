@@ -352,13 +352,14 @@ def test_beyond_two_to_the_31_elements():
     torch.cuda.empty_cache()
 
 
-def test_graph_capture_replays():
+@pytest.mark.parametrize("kernel", ["per-element", "table"])
+def test_graph_capture_replays(kernel):
     # forward + backward captured into a graph after one eager call (which
     # builds the per-device output tables), replayed several times with
     # eager work and synchronisation in between; every replay must equal
-    # the eager result bit for bit
+    # the eager result bit for bit.  Both fp16 / bf16 forward kernels.
     rng = np.random.default_rng(31)
-    n = 3 * 65536 + 77
+    n = 3 * 65536 + 77 if kernel == "per-element" else P.fwd16_table_min() + 3 * 65536 + 77
     spec, table = golden_table("gelu_bf16_lm_ffn_16x2048x8192/b3")
     x = upload(O.round_array(O.BF16, rng.normal(0, 2, n)), "bf16")
     g = upload(O.round_array(O.BF16, rng.normal(0, 1, n)), "bf16")
