@@ -392,7 +392,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": w.dtype,
+        # arithmetic of the path: f, the compares and the gradient products in
+        # fp32 (the 16-bit forward looks up outputs evaluated in fp32);
+        # tensors are stored in the workload's type
+        "dtype": "f32",
+        "storage_dtype": w.dtype,
         "data": "synthetic (seeded numpy draws, see workloads.py)",
         "config": {
             "workload": f"{w.name}: {w.act.upper()} {bits}-bit {w.dtype} {list(w.shape)}",
