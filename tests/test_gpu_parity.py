@@ -388,6 +388,18 @@ def test_graph_capture_replays(kernel):
         assert torch.equal(gin2.view(torch.int16), gin_ref.view(torch.int16)), rep
 
 
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+def test_empty_tensors(dt):
+    # n = 0 launches nothing and returns empty results
+    from parity import torch_dtype
+    s, v, table = _synthetic_table("gelu", 3)
+    x = torch.empty(0, dtype=torch_dtype(dt), device="cuda")
+    y, codes = P.fwd(table, x)
+    gin = P.bwd(table, x, codes)
+    torch.cuda.synchronize()
+    assert y.numel() == 0 and gin.numel() == 0 and P.packed_words(0, 3) == 0
+
+
 def test_misaligned_pointer_is_rejected():
     s, v, table = _synthetic_table("gelu", 3)
     x = torch.zeros(1000, dtype=torch.bfloat16, device="cuda")
