@@ -35,10 +35,12 @@
  *                             y[idx] (Listing 1, backward).
  *   refinement             -- Sec. 3: y(s) by Eq. (4), the analytic gradient
  *                             of L(s, y(s)) in s, gradient descent from the
- *                             DP result (reading R9).
+ *                             DP result (reading R14).
  *
  * Readings where the paper is silent or garbled (each one is listed in the
- * design notes of the repository):
+ * design notes of the repository, whose numbering these keep; R9-R13 there
+ * concern the GELU variant, the symmetric fit, the code layout and the
+ * workloads, and are stated at the functions they shape):
  *   R1  Eq. (7) prints the same k on both sides of the recurrence; it is read
  *       as DP(i,k+1) = min_{j<i} DP(j,k) + T(j,i), matching Eq. (6).
  *   R2  Eq. (6) prints y(t',t) without the normalising integral of w; it is
@@ -57,7 +59,7 @@
  *       boundaries s_m <= x.  NaN compares false (idx 0); -0 == +0.
  *   R8  Half-precision gradients are rounded twice by definition: the fp32
  *       product widen(g)*v[idx], then round-to-nearest-even to the dtype.
- *   R9  The paper leaves the gradient method open; the refinement here is
+ *   R14 The paper leaves the gradient method open; the refinement here is
  *       steepest descent with Armijo backtracking, integrals at off-grid
  *       boundaries taken as the grid prefix plus the partial cell by the
  *       same 8-point rule.
