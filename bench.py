@@ -12,6 +12,7 @@ algorithmic bytes: forward reads x (s bytes) and writes y (s) and codes
 (b/8); backward reads grad_out (s) and codes (b/8) and writes grad_in (s).
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--bits B]
+  python bench.py --sweep [--sweep-n N]        (every activation x type x bits)
   python bench.py --summarize-trace DIR [--summarize-counters FETCH_DIR WRITE_DIR]
 """
 import argparse
@@ -257,6 +258,50 @@ def cpu_baseline(w, bits, x_np, g_np, seconds=10.0, chunk=1 << 22):
     }
 
 
+def sweep(n: int, steps: int, warmup: int) -> None:
+    """Forward and backward of every activation x storage type x bit width on
+    n seeded synthetic elements (x ~ N(0, 3^2), grad_out ~ N(0, 1)), tables
+    fitted under N(0, 3^2) on [-30, 30]; HIP events on the launch stream,
+    inputs resident in HBM.  One JSON line per combination."""
+    import numpy as np
+    import torch
+    import paper_2202_00441_amd as P
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    gen = torch.Generator(device=dev).manual_seed(5)
+    x32 = torch.randn(n, device=dev, generator=gen) * 3.0
+    g32 = torch.randn(n, device=dev, generator=gen)
+    stream = torch.cuda.current_stream()
+    for dtype, tdt in (("f32", torch.float32), ("f16", torch.float16), ("bf16", torch.bfloat16)):
+        x, g = x32.to(tdt), g32.to(tdt)
+        y, gin = torch.empty_like(x), torch.empty_like(g)
+        for act in ("gelu", "silu", "sigmoid", "tanh", "relu", "selu", "softplus"):
+            for bits in (1, 2, 3, 4):
+                table = P.fit_table(act, bits, P.Weight(P.W_NORMAL, -30.0, 30.0, 0.0, 3.0), 2000)
+                codes = torch.empty(P.packed_words(n, bits), dtype=torch.int32, device=dev)
+                for _ in range(warmup):
+                    P.fwd(table, x, y=y, codes=codes)
+                    P.bwd(table, g, codes, grad_in=gin)
+                ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+                torch.cuda.synchronize()
+                for k in range(steps):
+                    ev[k][0].record(stream)
+                    P.fwd(table, x, y=y, codes=codes)
+                    ev[k][1].record(stream)
+                    P.bwd(table, g, codes, grad_in=gin)
+                    ev[k][2].record(stream)
+                torch.cuda.synchronize()
+                fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+                bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+                b = algorithmic_bytes(n, dtype, bits)
+                print(json.dumps({
+                    "act": act, "dtype": dtype, "bits": bits, "n": n,
+                    "fwd_kernel": kernel_name("fwd", dtype, bits, act, n, P.fwd16_table_min()),
+                    "fwd_ms": round(fwd_ms, 5), "fwd_frac_peak": round(b / (fwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                    "bwd_ms": round(bwd_ms, 5), "bwd_frac_peak": round(b / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -269,6 +314,10 @@ def main():
     ap.add_argument("--memory", action="store_true",
                     help="report activation memory held for backward, vanilla vs few-bit, on a "
                          "GPT-2-small-shaped stack of feed-forward blocks, instead of timing")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time forward and backward for every activation, storage type and bit "
+                         "width on --sweep-n elements (one JSON line each) instead of the headline")
+    ap.add_argument("--sweep-n", type=int, default=1 << 26)
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="summarise a rocprofv3 --kernel-trace --stats output directory")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -308,6 +357,10 @@ def main():
                                    "d_ff 3072 (GPT-2 small), 8 x 256 tokens, random weights"},
             "rows": rows,
         }), flush=True)
+        return
+
+    if args.sweep:
+        sweep(args.sweep_n, args.steps, args.warmup)
         return
 
     w = WL.WORKLOADS[args.workload]
