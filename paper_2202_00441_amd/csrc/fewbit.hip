@@ -699,10 +699,14 @@ __device__ void build_code_table(uint8_t* clut, const TableArgs& tab, int symmet
   constexpr uint32_t kSeg = 65536u / FEWBIT_FWD16_THREADS;
   static_assert(kSeg >= 32 && kSeg <= 32768 && 65536u % FEWBIT_FWD16_THREADS == 0,
                 "segments of whole 16-byte stores within one sign");
-  const Bounds bd = bounds_of(tab);
+  // every call below is made by all 64 lanes of the wave, as Search's
+  // permutes require: the segment loop takes two patterns per lane and kSeg
+  // is a multiple of 128, so all lanes run it equally often
+  static_assert(kSeg % (2 * kWave) == 0, "whole waves in the segment loop");
+  const Search<BITS> cl(tab, static_cast<int>(threadIdx.x & (kWave - 1)));
   auto code_of = [&](uint32_t p) {
     const float v = Half<DT>::widen(p);
-    return classify<BITS>(symmetric ? fabsf(v) : v, bd);
+    return cl(symmetric ? fabsf(v) : v);
   };
   const uint32_t p0 = threadIdx.x * kSeg;
   const uint32_t last = p0 + kSeg - 1u;
@@ -710,8 +714,8 @@ __device__ void build_code_table(uint8_t* clut, const TableArgs& tab, int symmet
   // whose two ends agree is uniform, unless it reaches the infinities and
   // NaNs at the top of its sign (exponent all ones)
   const bool special = (last & 0x7FFFu) >= Half<DT>::kSpecialFrom;
-  const uint32_t a = code_of(p0);
-  const bool uniform = !special && a == code_of(last);
+  const uint32_t a = code_of(p0), b = code_of(last);
+  const bool uniform = !special && a == b;
   if (uniform) {
     const uint32_t rep = a * 0x11111111u;
 #pragma unroll
