@@ -190,6 +190,45 @@ def test_table_kernel_every_activation(act, dt):
         _run_synthetic(act, bits, dt, x, g, f"table kernel {act}")
 
 
+# Every one of the 65536 fp16 / bf16 input patterns (NaNs, infinities,
+# subnormals and both zeros included) through both forward kernels: the
+# per-element one on one shuffled copy of the pattern set, the table one on
+# shuffled copies filling fwd16_table_min() + 77 elements, so that every
+# entry of the LDS output and code tables is read and checked.  All bit
+# widths, and for the even f' of Sigmoid and Tanh also the |x| tables.
+@pytest.mark.parametrize("act", ["gelu", "silu", "sigmoid", "tanh"] + MORE_ACTS)
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+def test_every_input_pattern(act, dt):
+    rng = np.random.default_rng(41)
+    pats = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    sizes = {"per-element": pats.size + 77, "table": P.fwd16_table_min() + 77}
+    cases = [(b, False) for b in (1, 2, 3, 4)]
+    if act in ("sigmoid", "tanh"):
+        cases += [(b, True) for b in (1, 2, 3, 4)]
+    for bits, sym in cases:
+        if sym:
+            F = O.fit(OACT[act], bits, O.uniform(-8.0, 8.0), 400, symmetric=True)
+            s, v = F.s, F.v
+            table = P.Table.from_values(P.ACTS[act], bits, s, v, flags=P.FLAG_SYMMETRIC)
+        else:
+            s, v, table = _synthetic_table(act, bits)
+        for kernel, n in sizes.items():
+            reps = -(-n // pats.size)
+            x_bits = np.concatenate([rng.permutation(pats) for _ in range(reps)])[:n]
+            g_bits = O.round_array(ODT[dt], rng.normal(0, 1, n))
+            label = f"every pattern {act} {dt} b{bits}{' sym' if sym else ''} {kernel} n={n}"
+            print(f"[patterns] {label}", flush=True)
+            y_ref, c_ref = O.fwd(OACT[act], ODT[dt], bits, s, x_bits, symmetric=sym,
+                                 threads=THREADS)
+            gin_ref = O.bwd(ODT[dt], bits, v, g_bits, c_ref, threads=THREADS)
+            y, codes = P.fwd(table, upload(x_bits, dt))
+            gin = P.bwd(table, upload(g_bits, dt), codes)
+            torch.cuda.synchronize()
+            check_exact(download_codes(codes)[:P.packed_words(n, bits)], c_ref, f"{label} codes")
+            check_y(download(y, dt), y_ref, dt, f"{label} y")
+            check_exact(download(gin, dt), gin_ref, f"{label} grad_in")
+
+
 # Symmetric tables (Fig. 3 caption: an even f' is fitted on [0, B] and the
 # bins apply to |x|), fitted by the oracle for the Sigmoid and Tanh inputs.
 SYM = sorted((k.split("/")[0], int(k.split("/")[1][1:])) for k in TABLES if k.endswith("/sym"))
