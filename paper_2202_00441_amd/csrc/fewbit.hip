@@ -461,14 +461,15 @@ __device__ inline uint32_t classify(float x, const Bounds& bd) {
   return idx;
 }
 
-// The classification of the per-element kernels.  Up to 3 bits it is the
-// select tree above.  At 4 bits the tree's last level alone takes 7 selects,
-// so there the boundaries are spread over the lanes of one register (lane i
-// holds s[i], i < 15): the first level compares with the middle boundary,
-// held in a scalar register, and each later level reads its boundary from
-// the lane the search has reached with one cross-lane permute (ds_bpermute),
-// ~3 VALU operations and one permute per level.  All 64 lanes must take part
-// in every call (the permutes read other lanes).
+// The classification of the per-element kernels and of the code-table
+// build.  Up to 3 bits it is the select tree above.  At 4 bits the tree's
+// last level alone takes 7 selects, so there the boundaries are spread over
+// the lanes of one register (lane i holds s[i], i < 15): the first level
+// compares with the middle boundary, held in a scalar register, and each
+// later level reads its boundary from the lane the search has reached with
+// one cross-lane permute (ds_bpermute), ~3 VALU operations and one permute
+// per level.  All 64 lanes must take part in every call (the permutes read
+// other lanes).
 template <int BITS>
 struct Search {
   static constexpr uint32_t K = 1u << BITS;
@@ -1191,8 +1192,7 @@ TableArgs table_args(const fewbit_table* t) {
   return a;
 }
 
-// Compute units of the current device, cached per device (the only state the
-// library keeps).
+// Compute units of the current device, read once per device.
 int device_cus() {
   static std::atomic<int> cache[64];
   int dev = 0;
@@ -1212,15 +1212,20 @@ int device_cus() {
 
 // Workgroups for n elements when each has `waves_per_block` streaming waves
 // that take `unroll` tiles per loop trip: one tile group per wave at most,
-// capped at wg_per_cu per compute unit when wg_per_cu > 0.
+// capped at wg_per_cu per compute unit when wg_per_cu > 0, and at 2^30
+// workgroups in any case (beyond 2^42 or so elements, far more than device
+// memory holds); every kernel's waves walk the tile groups, so a capped grid
+// still covers all of them.
 dim3 grid_for(int64_t n, int waves_per_block, int wg_per_cu, int unroll) {
-  const int64_t tiles = (n + kTile - 1) / kTile;
+  constexpr int64_t kMaxBlocks = int64_t{1} << 30;
+  const int64_t tiles = n / kTile + (n % kTile != 0);
   const int64_t groups = (tiles + unroll - 1) / unroll;
   int64_t blocks = (groups + waves_per_block - 1) / waves_per_block;
   if (wg_per_cu > 0) {
     const int64_t cap = static_cast<int64_t>(device_cus()) * wg_per_cu;
     if (blocks > cap) blocks = cap;
   }
+  if (blocks > kMaxBlocks) blocks = kMaxBlocks;
   if (blocks < 1) blocks = 1;
   return dim3(static_cast<unsigned>(blocks));
 }
@@ -1277,7 +1282,7 @@ struct Launch {
 
 template <int DT, int BITS, int ACT>
 void launch_fwd(const Launch& L) {
-  const int64_t nw = (L.n * BITS + 31) / 32;
+  const int64_t nw = fewbit_packed_words(L.n, BITS);
   const int sym = (L.t->flags & FEWBIT_FLAG_SYMMETRIC) ? 1 : 0;
   if constexpr (DT == FEWBIT_F32) {
     const dim3 grid = grid_for(L.n, FEWBIT_FWD32_THREADS / kWave, FEWBIT_FWD32_WG_PER_CU, FEWBIT_FWD32_UNROLL);
@@ -1325,7 +1330,7 @@ void launch_fwd_bits(const Launch& L) {
 
 template <int DT, int BITS>
 void launch_bwd(const Launch& L) {
-  const int64_t nw = (L.n * BITS + 31) / 32;
+  const int64_t nw = fewbit_packed_words(L.n, BITS);
   (void)hipGetLastError();
   if constexpr (DT == FEWBIT_F32) {
     const dim3 grid = grid_for(L.n, FEWBIT_BWD32_THREADS / kWave, FEWBIT_BWD_WG_PER_CU, FEWBIT_BWD32_UNROLL);

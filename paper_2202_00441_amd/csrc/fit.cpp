@@ -354,5 +354,6 @@ extern "C" int fewbit_fit_table(int32_t act, int32_t bits, const fewbit_weight* 
 
 extern "C" int64_t fewbit_packed_words(int64_t n, int32_t bits) {
   if (n < 0 || bits < 1 || bits > 4) return -1;
-  return (n * bits + 31) / 32;
+  // ceil(n * bits / 32) without forming n * bits, which overflows near 2^63
+  return (n / 32) * bits + ((n % 32) * bits + 31) / 32;
 }

@@ -50,6 +50,10 @@ def test_packed_words():
         for n in (0, 1, 31, 32, 33, 1000, 67108863, 268435456):
             assert P.packed_words(n, bits) == (n * bits + 31) // 32 == O.packed_words(n, bits)
     assert P.packed_words(-1, 3) == -1
+    # no overflow up to the largest count the type holds
+    for n in (2 ** 61, 2 ** 62 + 5, 2 ** 63 - 1):
+        for bits in (1, 2, 3, 4):
+            assert P.packed_words(n, bits) == (n * bits + 31) // 32
     assert P.packed_words(10, 0) == -1 and P.packed_words(10, 5) == -1
 
 
