@@ -66,11 +66,6 @@
 #ifndef FEWBIT_FWD16_UNROLL
 #define FEWBIT_FWD16_UNROLL 4
 #endif
-// waves per fp16 / bf16 forward workgroup that stream after the tables are
-// built (all of them build the tables; the rest then exit)
-#ifndef FEWBIT_FWD16_STREAM_WAVES
-#define FEWBIT_FWD16_STREAM_WAVES (FEWBIT_FWD16_THREADS / 64)
-#endif
 // the fp16 / bf16 forward by evaluation (no tables): threads per workgroup,
 // and the element count from which the table kernel is used instead
 #ifndef FEWBIT_FWD16V_THREADS
@@ -610,20 +605,20 @@ struct WaveIndex {
   int lane;
   int64_t wave, nwaves;
 };
-// Waves 0 .. per_block-1 of every workgroup, numbered across the grid.
-__device__ inline WaveIndex wave_index_of(int per_block) {
+// The waves of every workgroup, numbered across the grid.  The waves per
+// workgroup come from the launch's THREADS as a compile-time constant:
+// blockDim would be a vector load from the dispatch packet, waited for
+// before the first stream load.
+template <int THREADS>
+__device__ inline WaveIndex wave_index() {
+  constexpr int kPerBlock = THREADS / kWave;
   // the wave's number within its workgroup is the same in all its lanes;
   // readfirstlane tells the compiler so, which keeps tile addresses scalar
   const int w = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
   return {static_cast<int>(threadIdx.x & (kWave - 1)),
-          static_cast<int64_t>(blockIdx.x) * per_block + w,
-          static_cast<int64_t>(gridDim.x) * per_block};
+          static_cast<int64_t>(blockIdx.x) * kPerBlock + w,
+          static_cast<int64_t>(gridDim.x) * kPerBlock};
 }
-// The launch's waves per workgroup as a compile-time constant: blockDim
-// would be a vector load from the dispatch packet, waited for before the
-// first stream load.
-template <int THREADS>
-__device__ inline WaveIndex wave_index() { return wave_index_of(THREADS / kWave); }
 
 // ---------------------------------------------------------------- forward, fp16 / bf16
 // For 16-bit inputs both results of the forward are functions of the input
@@ -769,10 +764,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   __builtin_amdgcn_s_waitcnt(0);     // the table loads have landed in LDS
   __syncthreads();
 
-  constexpr int kStream = FEWBIT_FWD16_STREAM_WAVES;
-  static_assert(kStream >= 1 && kStream <= FEWBIT_FWD16_THREADS / kWave, "stream waves");
-  if (static_cast<int>(threadIdx.x / kWave) >= kStream) return;   // no barrier follows
-  const WaveIndex wi = wave_index_of(kStream);
+  const WaveIndex wi = wave_index<FEWBIT_FWD16_THREADS>();
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
@@ -1297,7 +1289,7 @@ void launch_fwd(const Launch& L) {
                        static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
                        L.n, nw, table_args(L.t), sym);
   } else {
-    const dim3 grid = grid_for(L.n, FEWBIT_FWD16_STREAM_WAVES, FEWBIT_FWD16_WG_PER_CU, FEWBIT_FWD16_UNROLL);
+    const dim3 grid = grid_for(L.n, FEWBIT_FWD16_THREADS / kWave, FEWBIT_FWD16_WG_PER_CU, FEWBIT_FWD16_UNROLL);
     (void)hipGetLastError();
     hipLaunchKernelGGL((fwd16_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16_THREADS), 0, L.s,
                        static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
