@@ -196,6 +196,9 @@ def test_table_kernel_every_activation(act, dt):
 # shuffled copies filling fwd16_table_min() + 77 elements, so that every
 # entry of the LDS output and code tables is read and checked.  All bit
 # widths, and for the even f' of Sigmoid and Tanh also the |x| tables.
+# Both kernels evaluate the same f with the same rounding, so beyond the
+# oracle's tolerance their outputs must agree bit for bit, pattern by
+# pattern.
 @pytest.mark.parametrize("act", ["gelu", "silu", "sigmoid", "tanh"] + MORE_ACTS)
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 def test_every_input_pattern(act, dt):
@@ -212,6 +215,7 @@ def test_every_input_pattern(act, dt):
             table = P.Table.from_values(P.ACTS[act], bits, s, v, flags=P.FLAG_SYMMETRIC)
         else:
             s, v, table = _synthetic_table(act, bits)
+        y_of_pattern = {}
         for kernel, n in sizes.items():
             reps = -(-n // pats.size)
             x_bits = np.concatenate([rng.permutation(pats) for _ in range(reps)])[:n]
@@ -227,6 +231,13 @@ def test_every_input_pattern(act, dt):
             check_exact(download_codes(codes)[:P.packed_words(n, bits)], c_ref, f"{label} codes")
             check_y(download(y, dt), y_ref, dt, f"{label} y")
             check_exact(download(gin, dt), gin_ref, f"{label} grad_in")
+            y_bits = download(y, dt)
+            by_pattern = np.zeros(pats.size, np.uint16)
+            by_pattern[x_bits] = y_bits
+            check_exact(by_pattern[x_bits], y_bits, f"{label}: one y per pattern")
+            y_of_pattern[kernel] = by_pattern
+        check_exact(y_of_pattern["table"], y_of_pattern["per-element"],
+                    f"every pattern {act} {dt} b{bits}: table vs per-element y")
 
 
 # Symmetric tables (Fig. 3 caption: an even f' is fitted on [0, B] and the
