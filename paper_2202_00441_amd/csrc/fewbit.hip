@@ -376,8 +376,21 @@ constexpr float kSeluLambdaAlpha = 1.7580993408473766f;
 
 template <int DT>
 struct Act<DT, FEWBIT_SELU> {
+  // (the 16-bit output tables, evaluated once per device)
   __device__ static float f(float x) {
     return x > 0.0f ? kSeluLambda * x : kSeluLambdaAlpha * expm1f(x);   // NaN via expm1f
+  }
+};
+template <>
+struct Act<FEWBIT_F32, FEWBIT_SELU> {
+  // e^x - 1 from the hardware exponential: near 0 the subtraction cancels,
+  // so the error is an absolute one of about 2^-23 (times lambda alpha), not
+  // a relative one; the fp32 results stay well inside their tolerance.  The
+  // libm form above keeps the relative accuracy that fp16 outputs near 0
+  // need.  NaN via the exponential, -inf gives -lambda alpha.
+  __device__ static float f(float x) {
+    const float e = __builtin_amdgcn_exp2f(x * kLog2e);
+    return x > 0.0f ? kSeluLambda * x : kSeluLambdaAlpha * (e - 1.0f);
   }
 };
 
@@ -472,7 +485,9 @@ struct Search {
   Bounds bd;          // the select tree's boundaries (BITS <= 3)
   float mid;          // s[K/2 - 1]
   int lane_bound;     // s[lane] for lane < 15
-  __device__ Search(const TableArgs& tab, int lane) : bd(bounds_of(tab)) {
+  uint32_t keep;      // bits of x that are classified: all, or all but the sign
+  __device__ Search(const TableArgs& tab, int lane, int symmetric)
+      : bd(bounds_of(tab)), keep(symmetric ? 0x7FFFFFFFu : 0xFFFFFFFFu) {
     float v = 0.0f;
 #pragma unroll
     for (int m = 0; m < 15; ++m) {
@@ -481,18 +496,23 @@ struct Search {
     }
     lane_bound = __float_as_int(v);
   }
+  // the index of x, or of |x| for a symmetric table (one AND with the mask:
+  // -0 becomes +0 and a NaN stays a NaN, as with fabsf)
+  __device__ uint32_t code(float x) const { return (*this)(__uint_as_float(__float_as_uint(x) & keep)); }
   __device__ uint32_t operator()(float x) const {
     if constexpr (!kPermute) {
       return classify<BITS>(x, bd);
     } else {
-      uint32_t idx = x >= mid ? K / 2 : 0u;
+      // a = 4 idx, the byte address ds_bpermute takes; the constant part of
+      // each level's address goes into the instruction's offset field
+      uint32_t a = x >= mid ? 4u * (K / 2) : 0u;
 #pragma unroll
       for (uint32_t step = K / 4; step >= 1; step /= 2) {
         const float b = __int_as_float(
-            __builtin_amdgcn_ds_bpermute(static_cast<int>((idx + step - 1) << 2), lane_bound));
-        idx += x >= b ? step : 0u;
+            __builtin_amdgcn_ds_bpermute(static_cast<int>(a + 4u * (step - 1)), lane_bound));
+        a += x >= b ? 4u * step : 0u;
       }
-      return idx;
+      return a >> 2;
     }
   }
 };
@@ -699,11 +719,8 @@ __device__ void build_code_table(uint8_t* clut, const TableArgs& tab, int symmet
   // permutes require: the segment loop takes two patterns per lane and kSeg
   // is a multiple of 128, so all lanes run it equally often
   static_assert(kSeg % (2 * kWave) == 0, "whole waves in the segment loop");
-  const Search<BITS> cl(tab, static_cast<int>(threadIdx.x & (kWave - 1)));
-  auto code_of = [&](uint32_t p) {
-    const float v = Half<DT>::widen(p);
-    return cl(symmetric ? fabsf(v) : v);
-  };
+  const Search<BITS> cl(tab, static_cast<int>(threadIdx.x & (kWave - 1)), symmetric);
+  auto code_of = [&](uint32_t p) { return cl.code(Half<DT>::widen(p)); };
   const uint32_t p0 = threadIdx.x * kSeg;
   const uint32_t last = p0 + kSeg - 1u;
   // the index is monotone in the pattern within one sign, so a segment
@@ -817,11 +834,10 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
 // y and the two codes of the element pair in word w; the codes go to bits
 // shift .. shift + 2*BITS - 1 of F.
 template <int DT, int BITS, int ACT>
-__device__ inline uint32_t fwd16v_pair(uint32_t w, const Search<BITS>& cl, int symmetric, uint32_t& F,
-                                       int shift) {
+__device__ inline uint32_t fwd16v_pair(uint32_t w, const Search<BITS>& cl, uint32_t& F, int shift) {
   using H = Half<DT>;
   const float a = H::lo(w), b = H::hi(w);
-  F |= (cl(symmetric ? fabsf(a) : a) << shift) | (cl(symmetric ? fabsf(b) : b) << (shift + BITS));
+  F |= (cl.code(a) << shift) | (cl.code(b) << (shift + BITS));
   return H::pack(Act<DT, ACT>::f(a), Act<DT, ACT>::f(b));
 }
 
@@ -831,7 +847,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16V_THREADS) void fwd16v_kernel(
     TableArgs tab, int symmetric) {
   constexpr int kWords = 16 * BITS;
   const WaveIndex wi = wave_index<FEWBIT_FWD16V_THREADS>();
-  const Search<BITS> cl(tab, wi.lane);
+  const Search<BITS> cl(tab, wi.lane, symmetric);
   const int64_t full = n / kTile;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
   const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
@@ -840,7 +856,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16V_THREADS) void fwd16v_kernel(
     u32x4_t out;
     uint32_t F = 0;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) out[k] = fwd16v_pair<DT, BITS, ACT>(in[k], cl, symmetric, F, 2 * k * BITS);
+    for (int k = 0; k < 4; ++k) out[k] = fwd16v_pair<DT, BITS, ACT>(in[k], cl, F, 2 * k * BITS);
     Span(y + t * kTile, kSpanBytes).st16(lane_b, out);
     pack_store_full<BITS>(Span(codes + t * kWords, kWords * 4), F, wi.lane);
   }
@@ -852,7 +868,7 @@ __global__ __launch_bounds__(FEWBIT_FWD16V_THREADS) void fwd16v_kernel(
     for (int j = 0; j < kPerLane; ++j) {
       const int64_t e = t * kTile + lane_off + j;
       const float v = e < n ? Half<DT>::widen(x[e]) : 0.0f;
-      const uint32_t c = cl(symmetric ? fabsf(v) : v);       // all lanes
+      const uint32_t c = cl.code(v);                          // all lanes
       if (e < n) {
         y[e] = static_cast<uint16_t>(Half<DT>::pack(Act<DT, ACT>::f(v), 0.0f) & 0xFFFFu);
         F |= c << (BITS * j);
@@ -921,14 +937,13 @@ __device__ inline uint32_t load_field32(const Span& base, int v, int lane, int64
 
 // ---------------------------------------------------------------- forward, fp32
 template <int BITS, int ACT>
-__device__ inline void fwd32_half(u32x4_t in, const Search<BITS>& cl, int symmetric, u32x4_t& out,
-                                  uint32_t& f) {
+__device__ inline void fwd32_half(u32x4_t in, const Search<BITS>& cl, u32x4_t& out, uint32_t& f) {
   f = 0;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const float xv = __uint_as_float(in[j]);
     out[j] = __float_as_uint(Act<FEWBIT_F32, ACT>::f(xv));
-    f |= cl(symmetric ? fabsf(xv) : xv) << (BITS * j);
+    f |= cl.code(xv) << (BITS * j);
   }
 }
 
@@ -939,7 +954,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
   constexpr int U = FEWBIT_FWD32_UNROLL;
   constexpr int kWords = Codes32<BITS>::kWords;
   const WaveIndex wi = wave_index<FEWBIT_FWD32_THREADS>();
-  const Search<BITS> cl(tab, wi.lane);
+  const Search<BITS> cl(tab, wi.lane, symmetric);
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * 4;
@@ -956,7 +971,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) fwd32_half<BITS, ACT>(in[u][h], cl, symmetric, out[u][h], f[u][h]);
+      for (int h = 0; h < 2; ++h) fwd32_half<BITS, ACT>(in[u][h], cl, out[u][h], f[u][h]);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
 #pragma unroll
@@ -969,8 +984,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
     uint32_t f[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      fwd32_half<BITS, ACT>(Span(x + t * kTile + h * 256, kSpanBytes).ld16(lane_b), cl, symmetric,
-                            out[h], f[h]);
+      fwd32_half<BITS, ACT>(Span(x + t * kTile + h * 256, kSpanBytes).ld16(lane_b), cl, out[h], f[h]);
       Span(y + t * kTile + h * 256, kSpanBytes).st16(lane_b, out[h]);
     }
     pack_store32<BITS, true>(Span(codes + t * kWords, kWords * 4), f[0], f[1], wi.lane, kWords);
@@ -985,7 +999,7 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
       for (int j = 0; j < 4; ++j) {
         const int64_t e = t * kTile + h * 256 + lane_off + j;
         const float xv = e < n ? x[e] : 0.0f;
-        const uint32_t c = cl(symmetric ? fabsf(xv) : xv);  // all lanes
+        const uint32_t c = cl.code(xv);                     // all lanes
         if (e < n) {
           y[e] = Act<FEWBIT_F32, ACT>::f(xv);
           f[h] |= c << (BITS * j);
