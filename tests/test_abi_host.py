@@ -100,6 +100,19 @@ def test_library_fit_matches_oracle_fit(key):
         assert np.allclose(T.v, F.v[::-1], rtol=0, atol=1e-6)
 
 
+@pytest.mark.parametrize("key", sorted(TABLES))
+def test_stored_tables_are_the_oracles_fit(key):
+    # tables.json is written by tests/golden/make_tables.py from the oracle
+    # alone: refitting with the oracle gives the stored bits back
+    spec = TABLES[key]
+    w = spec["weight"]
+    F = O.fit(ORACLE_ACT[spec["act"]], spec["bits"], _oracle_weight(w), w["n_grid"],
+              symmetric=bool(spec["symmetric"]))
+    assert [float(x).hex() for x in F.s] == spec["s"]
+    assert [float(x).hex() for x in F.v] == spec["v"]
+    assert F.loss == spec["loss"]
+
+
 @pytest.mark.parametrize("act,bits,sym", [("sigmoid", 3, True), ("tanh", 2, True),
                                           ("silu", 4, False), ("gelu", 1, False)])
 def test_library_fit_other_cases(act, bits, sym):
