@@ -225,6 +225,12 @@ def test_fit_argument_errors():
     cw = w.c()
     assert _lib.lib.fewbit_fit_table(0, 3, C.byref(cw), 100, 4, C.byref(ct)) == _lib.E_INVALID
     assert _lib.lib.fewbit_fit_table(0, 3, C.byref(cw), 100, 8, C.byref(ct)) == _lib.E_INVALID
+    # grid above 2^20 cells, a reserved field set, no output
+    assert _lib.lib.fewbit_fit_table(0, 3, C.byref(cw), (1 << 20) + 1, 0, C.byref(ct)) == _lib.E_INVALID
+    cw.reserved = 1
+    assert _lib.lib.fewbit_fit_table(0, 3, C.byref(cw), 100, 0, C.byref(ct)) == _lib.E_INVALID
+    cw.reserved = 0
+    assert _lib.lib.fewbit_fit_table(0, 3, C.byref(cw), 100, 0, None) == _lib.E_NULL
 
 
 def _table(bits=3):
@@ -273,6 +279,9 @@ def test_fwd_bwd_errors_before_launch():
     bad = _table()
     bad.c.flags = 2
     assert fwd(bad, P.F32, A, A, A, 10, 0) == _lib.E_INVALID
+    bad = _table()
+    bad.c.reserved = 1
+    assert bwd(bad, P.F32, A, A, A, 10, 0) == _lib.E_INVALID
     assert _lib.lib.fewbit_fwd(None, 0, A, A, A, 10, None) == _lib.E_NULL
 
 
