@@ -296,7 +296,7 @@ def sweep(n: int, steps: int, warmup: int) -> None:
                 b = algorithmic_bytes(n, dtype, bits)
                 print(json.dumps({
                     "act": act, "dtype": dtype, "bits": bits, "n": n,
-                    "fwd_kernel": kernel_name("fwd", dtype, bits, act, n, P.fwd16_table_min()),
+                    "fwd_kernel": kernel_name("fwd", dtype, bits, act, n, P.fwd16_table_min(act, bits)),
                     "fwd_ms": round(fwd_ms, 5), "fwd_frac_peak": round(b / (fwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                     "bwd_ms": round(bwd_ms, 5), "bwd_frac_peak": round(b / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                 }), flush=True)
@@ -471,7 +471,7 @@ def main():
         "copy_ceiling": {"GB/s": round(copy_gbps, 2), "ms": round(copy_ms, 5),
                          "what": "torch copy_ of x (read+write, same element count)"},
         "roofline": {
-            "kernel": kernel_name(dom, w.dtype, bits, w.act, n, P.fwd16_table_min()),
+            "kernel": kernel_name(dom, w.dtype, bits, w.act, n, P.fwd16_table_min(w.act, bits)),
             "bound": "hbm",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBPS,

@@ -24,12 +24,12 @@
  *   - Global state, per device: the compute-unit count (read once, it sizes
  *     the launch grid) and, for the fp16 / bf16 forward, static device
  *     tables of f over all 65536 input patterns of each activation and
- *     type (1.75 MiB of module memory).  The first fp16 / bf16 fewbit_fwd on
- *     a device with n >= fewbit_fwd16_table_min() evaluates those tables on
- *     a private non-blocking stream and waits for that stream alone; it
- *     therefore must not be made while a stream is being captured into a
- *     graph in a mode that forbids synchronisation.  Calls are reentrant
- *     and thread-safe.
+ *     type (1.75 MiB of module memory).  The first fp16 / bf16 fewbit_fwd
+ *     on a device with n >= fewbit_fwd16_table_min(act, bits) evaluates
+ *     those tables on a private non-blocking stream and waits for that
+ *     stream alone; it therefore must not be made while a stream is being
+ *     captured into a graph in a mode that forbids synchronisation.  Calls
+ *     are reentrant and thread-safe.
  *   - No C++ exception crosses this interface.
  */
 #ifndef FEWBIT_H
@@ -169,12 +169,15 @@ int64_t fewbit_packed_words(int64_t n, int32_t bits);
 int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, void* y,
                uint32_t* codes, int64_t n, void* stream);
 
-/* Element count from which an fp16 / bf16 forward runs the table kernel
- * (outputs and indices looked up per input bit pattern); smaller forwards
- * evaluate f and the compares per element.  Both give the same results;
- * this only tells a caller (or a test) which kernel a given n reaches.
- * Host only, no device access. */
-int64_t fewbit_fwd16_table_min(void);
+/* Element count from which an fp16 / bf16 forward of activation `act` at
+ * `bits` bits runs the table kernel (outputs and indices looked up per input
+ * bit pattern); smaller forwards evaluate f and the compares per element.
+ * INT64_MAX where the per-element kernel is used at every size (ReLU at 1
+ * and 2 bits, whose evaluation is cheap enough to stay bound by HBM).  Both
+ * kernels give the same results; this only tells a caller (or a test) which
+ * kernel a given n reaches.  Returns -1 for an unknown activation or bits
+ * outside 1..4.  Host only, no device access. */
+int64_t fewbit_fwd16_table_min(int32_t act, int32_t bits);
 
 /*
  * fewbit_bwd -- backward of the few-bit activation (Eq. (1) with f'(x)

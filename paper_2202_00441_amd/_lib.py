@@ -69,7 +69,7 @@ def _load():
     L.fewbit_bwd.restype = C.c_int
     L.fewbit_bwd.argtypes = [C.POINTER(CTable), i32, vp, vp, vp, i64, vp]
     L.fewbit_fwd16_table_min.restype = i64
-    L.fewbit_fwd16_table_min.argtypes = []
+    L.fewbit_fwd16_table_min.argtypes = [i32, i32]
     L.fewbit_strerror.restype = C.c_char_p
     L.fewbit_strerror.argtypes = [i32]
     return L
@@ -167,9 +167,15 @@ def packed_words(n: int, bits: int) -> int:
     return int(lib.fewbit_packed_words(int(n), int(bits)))
 
 
-def fwd16_table_min() -> int:
-    """Element count from which fp16 / bf16 forwards use the table kernel."""
-    return int(lib.fewbit_fwd16_table_min())
+def fwd16_table_min(act, bits: int) -> int:
+    """Element count from which fp16 / bf16 forwards of this activation and
+    bit width use the table kernel (2^63 - 1: never, the per-element kernel
+    runs at every size)."""
+    a = ACTS[act] if isinstance(act, str) else int(act)
+    r = int(lib.fewbit_fwd16_table_min(a, int(bits)))
+    if r < 0:
+        raise FewbitError(E_INVALID, "fewbit_fwd16_table_min")
+    return r
 
 
 # ---------------------------------------------------------------- raw pointers

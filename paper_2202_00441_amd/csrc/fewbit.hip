@@ -30,8 +30,9 @@
 // outputs (evaluated once per device by a table kernel) and the indices
 // (4 bits per pattern, built per launch from the boundaries).  A lookup
 // costs two LDS reads instead of an evaluation of f and the compares.
-// Smaller fp16 / bf16 forwards, and every fp32 forward, evaluate f and
-// search the boundaries per element.
+// Smaller fp16 / bf16 forwards, ReLU at 1 and 2 bits (see
+// table_kernel_used), and every fp32 forward evaluate f and search the
+// boundaries per element.
 //
 // The fitted table travels as kernel arguments (scalar registers); the
 // backward spreads the values over the lanes of one register and reads
@@ -829,8 +830,10 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
 // fp16 / bf16 forward by evaluation: f and the compares for every element,
 // no tables.  The table kernel above needs ~3 us of setup per launch and a
 // persistent grid; below FEWBIT_FWD16_TABLE_MIN elements this kernel, one
-// wave per tile with no setup, is faster.  Outputs are the table kernel's:
-// the tables hold this same f and rounding.
+// wave per tile with no setup, is faster, and so it is at every size where
+// f and the classification are cheap enough to leave it bound by HBM
+// (table_kernel_used).  Outputs are the table kernel's: the tables hold this
+// same f and rounding.
 // y and the two codes of the element pair in word w; the codes go to bits
 // shift .. shift + 2*BITS - 1 of F.
 template <int DT, int BITS, int ACT>
@@ -1286,6 +1289,22 @@ struct Launch {
   hipStream_t s;
 };
 
+// Whether an fp16 / bf16 forward of (act, bits) uses the table kernel from
+// FEWBIT_FWD16_TABLE_MIN elements on.  ReLU at 1 or 2 bits does not: its f
+// is a select and its classification one or two compares, so the
+// per-element kernel stays bound by HBM and, as a one-wave-per-tile grid,
+// streams faster than the persistent table kernel at every size (about 79%
+// against 73% of the HBM peak at 1 bit, 76% against 73% at 2 bits).  For
+// every other activation and bit width the evaluation costs more than the
+// persistent grid does.
+constexpr bool table_kernel_used(int act, int bits) {
+  return !(act == FEWBIT_RELU && bits <= 2);
+}
+
+int64_t table_min_of(int act, int bits) {
+  return table_kernel_used(act, bits) ? FEWBIT_FWD16_TABLE_MIN : INT64_MAX;
+}
+
 template <int DT, int BITS, int ACT>
 void launch_fwd(const Launch& L) {
   const int64_t nw = fewbit_packed_words(L.n, BITS);
@@ -1296,18 +1315,21 @@ void launch_fwd(const Launch& L) {
     hipLaunchKernelGGL((fwd32_kernel<BITS, ACT>), grid, dim3(FEWBIT_FWD32_THREADS), 0, L.s,
                        static_cast<const float*>(L.in), static_cast<float*>(L.out), L.codes, L.n,
                        nw, table_args(L.t), sym);
-  } else if (L.n < FEWBIT_FWD16_TABLE_MIN) {
-    const dim3 grid = grid_for(L.n, FEWBIT_FWD16V_THREADS / kWave, 0, 1);
-    (void)hipGetLastError();
-    hipLaunchKernelGGL((fwd16v_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16V_THREADS), 0, L.s,
-                       static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
-                       L.n, nw, table_args(L.t), sym);
   } else {
-    const dim3 grid = grid_for(L.n, FEWBIT_FWD16_THREADS / kWave, FEWBIT_FWD16_WG_PER_CU, FEWBIT_FWD16_UNROLL);
-    (void)hipGetLastError();
-    hipLaunchKernelGGL((fwd16_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16_THREADS), 0, L.s,
-                       static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
-                       L.n, nw, table_args(L.t), sym);
+    constexpr bool kTable = table_kernel_used(ACT, BITS);
+    if (!kTable || L.n < FEWBIT_FWD16_TABLE_MIN) {
+      const dim3 grid = grid_for(L.n, FEWBIT_FWD16V_THREADS / kWave, 0, 1);
+      (void)hipGetLastError();
+      hipLaunchKernelGGL((fwd16v_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16V_THREADS), 0, L.s,
+                         static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
+                         L.n, nw, table_args(L.t), sym);
+    } else if constexpr (kTable) {
+      const dim3 grid = grid_for(L.n, FEWBIT_FWD16_THREADS / kWave, FEWBIT_FWD16_WG_PER_CU, FEWBIT_FWD16_UNROLL);
+      (void)hipGetLastError();
+      hipLaunchKernelGGL((fwd16_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16_THREADS), 0, L.s,
+                         static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
+                         L.n, nw, table_args(L.t), sym);
+    }
   }
 }
 
@@ -1386,7 +1408,7 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   if (misaligned(x) || misaligned(y) || misaligned(codes)) return FEWBIT_E_ALIGN;
   rc = check_stream_device(static_cast<hipStream_t>(stream));
   if (rc != FEWBIT_OK) return rc;
-  if (dtype != FEWBIT_F32 && n >= FEWBIT_FWD16_TABLE_MIN) {
+  if (dtype != FEWBIT_F32 && n >= table_min_of(t->act, t->bits)) {
     rc = ensure_output_tables();
     if (rc != FEWBIT_OK) return rc;
   }
@@ -1399,7 +1421,10 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   return launch_status("fewbit_fwd");
 }
 
-extern "C" int64_t fewbit_fwd16_table_min(void) { return FEWBIT_FWD16_TABLE_MIN; }
+extern "C" int64_t fewbit_fwd16_table_min(int32_t act, int32_t bits) {
+  if (act < FEWBIT_GELU || act > FEWBIT_SOFTPLUS || bits < 1 || bits > 4) return -1;
+  return table_min_of(act, bits);
+}
 
 extern "C" int fewbit_bwd(const fewbit_table* t, int32_t dtype, const void* grad_out,
                           const uint32_t* codes, void* grad_in, int64_t n, void* stream) {

@@ -123,7 +123,7 @@ int main(int argc, char** argv) {
   const fewbit_weight uniform{FEWBIT_W_UNIFORM, 0, -8.0, 8.0, 0.0, 1.0, 0.0, 1.0};
   // bf16 above the table-kernel size, on the null stream
   if (run_case(argv[1], "gelu_bf16_b3", FEWBIT_GELU, FEWBIT_BF16, 3, 0, normal,
-               fewbit_fwd16_table_min() + 1237, 3.0, nullptr))
+               fewbit_fwd16_table_min(FEWBIT_GELU, 3) + 1237, 3.0, nullptr))
     return 1;
   hipStream_t s;
   HIP_OK(hipStreamCreate(&s));

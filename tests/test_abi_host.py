@@ -40,9 +40,19 @@ def test_exports_every_declared_symbol():
 
 
 def test_fwd16_table_min():
-    # a positive element count, a whole number of 512-element tiles
-    m = P.fwd16_table_min()
+    # a positive element count, a whole number of 512-element tiles, the
+    # same for every activation and bit width that uses the table kernel
+    m = P.fwd16_table_min("gelu", 3)
     assert m > 0 and m % 512 == 0
+    for act in P.ACTS:
+        for bits in (1, 2, 3, 4):
+            expect = 2 ** 63 - 1 if (act == "relu" and bits <= 2) else m
+            assert P.fwd16_table_min(act, bits) == expect, (act, bits)
+    assert _lib.lib.fewbit_fwd16_table_min(7, 3) == -1
+    assert _lib.lib.fewbit_fwd16_table_min(0, 0) == -1
+    assert _lib.lib.fewbit_fwd16_table_min(0, 5) == -1
+    with pytest.raises(P.FewbitError):
+        P.fwd16_table_min(-1, 3)
 
 
 def test_packed_words():

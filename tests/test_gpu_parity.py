@@ -6,7 +6,7 @@ the benchmark runs, in its launch configuration), the same workloads cut to
 ragged lengths, an edge-size sweep over every dtype x bits x activation,
 special values, boundaries, ReLU / SELU / Softplus (Table 1's other rows),
 both fp16 / bf16 forward kernels (per-element evaluation below
-fwd16_table_min() elements, table lookups from there on),
+fwd16_table_min(act, bits) elements, table lookups from there on),
 the symmetric (|x|) tables of Sigmoid and Tanh,
 in-place aliasing, a second stream, canaries past every output, and the
 autograd wrapper.
@@ -168,17 +168,23 @@ def test_special_values_and_boundaries(act, dt):
     _run_synthetic(act, bits, dt, x, g, f"special {act}")
 
 
-# fp16 / bf16 forwards from fwd16_table_min() elements on run the table
-# kernel (LDS lookups per input bit pattern); smaller ones evaluate f and
-# the compares per element.  The cases above are mostly small; this one
-# takes every activation, half type and bit width through the table kernel,
-# with the special values and boundary neighbours in the mix.
+# fp16 / bf16 forwards from fwd16_table_min(act, bits) elements on run the
+# table kernel (LDS lookups per input bit pattern); smaller ones evaluate f
+# and the compares per element.  The cases above are mostly small; this one
+# takes every activation, half type and bit width that has a table kernel
+# through it (ReLU at 1 and 2 bits runs per element at every size), with
+# the special values and boundary neighbours in the mix.
+NEVER = 2 ** 63 - 1
+
+
 @pytest.mark.parametrize("act", ["gelu", "silu", "sigmoid", "tanh"] + MORE_ACTS)
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 def test_table_kernel_every_activation(act, dt):
-    n = P.fwd16_table_min() + 1234
     rng = np.random.default_rng(17)
     for bits in (1, 2, 3, 4):
+        if P.fwd16_table_min(act, bits) == NEVER:
+            continue
+        n = P.fwd16_table_min(act, bits) + 1234
         s, v, table = _synthetic_table(act, bits)
         special = O.round_array(ODT[dt], _special_values(dt, s))
         hb = O.round_array(ODT[dt], s.astype(np.float64))
@@ -198,13 +204,12 @@ def test_table_kernel_every_activation(act, dt):
 # widths, and for the even f' of Sigmoid and Tanh also the |x| tables.
 # Both kernels evaluate the same f with the same rounding, so beyond the
 # oracle's tolerance their outputs must agree bit for bit, pattern by
-# pattern.
+# pattern.  (ReLU at 1 and 2 bits has no table kernel: one size suffices.)
 @pytest.mark.parametrize("act", ["gelu", "silu", "sigmoid", "tanh"] + MORE_ACTS)
 @pytest.mark.parametrize("dt", ["f16", "bf16"])
 def test_every_input_pattern(act, dt):
     rng = np.random.default_rng(41)
     pats = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
-    sizes = {"per-element": pats.size + 77, "table": P.fwd16_table_min() + 77}
     cases = [(b, False) for b in (1, 2, 3, 4)]
     if act in ("sigmoid", "tanh"):
         cases += [(b, True) for b in (1, 2, 3, 4)]
@@ -215,6 +220,9 @@ def test_every_input_pattern(act, dt):
             table = P.Table.from_values(P.ACTS[act], bits, s, v, flags=P.FLAG_SYMMETRIC)
         else:
             s, v, table = _synthetic_table(act, bits)
+        sizes = {"per-element": pats.size + 77}
+        if P.fwd16_table_min(act, bits) != NEVER:
+            sizes["table"] = P.fwd16_table_min(act, bits) + 77
         y_of_pattern = {}
         for kernel, n in sizes.items():
             reps = -(-n // pats.size)
@@ -236,8 +244,9 @@ def test_every_input_pattern(act, dt):
             by_pattern[x_bits] = y_bits
             check_exact(by_pattern[x_bits], y_bits, f"{label}: one y per pattern")
             y_of_pattern[kernel] = by_pattern
-        check_exact(y_of_pattern["table"], y_of_pattern["per-element"],
-                    f"every pattern {act} {dt} b{bits}: table vs per-element y")
+        if "table" in y_of_pattern:
+            check_exact(y_of_pattern["table"], y_of_pattern["per-element"],
+                        f"every pattern {act} {dt} b{bits}: table vs per-element y")
 
 
 # Symmetric tables (Fig. 3 caption: an even f' is fitted on [0, B] and the
@@ -257,7 +266,7 @@ def test_symmetric_full_size(name, bits):
 @pytest.mark.parametrize("name,bits", SYM, ids=[f"{n}-b{b}" for n, b in SYM])
 def test_symmetric_half_types(name, bits, dt):
     w = WL.WORKLOADS[name]
-    for n in (1, 513, 4097, (1 << 20) + 3, P.fwd16_table_min() + 3):
+    for n in (1, 513, 4097, (1 << 20) + 3, P.fwd16_table_min(w.act, bits) + 3):
         x = WL.draw(w.x_dist, w.x_scale, n, dt, w.seed)
         g = WL.draw("normal", w.g_sigma, n, dt, w.seed + 1000)
         run_case(f"{name}/b{bits}/sym", dt, x, g, label=f"{name} b{bits} sym {dt} n={n}")
@@ -409,7 +418,7 @@ def test_graph_capture_replays(kernel):
     # eager work and synchronisation in between; every replay must equal
     # the eager result bit for bit.  Both fp16 / bf16 forward kernels.
     rng = np.random.default_rng(31)
-    n = 3 * 65536 + 77 if kernel == "per-element" else P.fwd16_table_min() + 3 * 65536 + 77
+    n = 3 * 65536 + 77 if kernel == "per-element" else P.fwd16_table_min("gelu", 3) + 3 * 65536 + 77
     spec, table = golden_table("gelu_bf16_lm_ffn_16x2048x8192/b3")
     x = upload(O.round_array(O.BF16, rng.normal(0, 2, n)), "bf16")
     g = upload(O.round_array(O.BF16, rng.normal(0, 1, n)), "bf16")
