@@ -199,7 +199,7 @@ def test_table_kernel_every_activation(act, dt):
 # Every one of the 65536 fp16 / bf16 input patterns (NaNs, infinities,
 # subnormals and both zeros included) through both forward kernels: the
 # per-element one on one shuffled copy of the pattern set, the table one on
-# shuffled copies filling fwd16_table_min() + 77 elements, so that every
+# shuffled copies filling fwd16_table_min(act, bits) + 77 elements, so that every
 # entry of the LDS output and code tables is read and checked.  All bit
 # widths, and for the even f' of Sigmoid and Tanh also the |x| tables.
 # Both kernels evaluate the same f with the same rounding, so beyond the
