@@ -367,8 +367,8 @@ struct Act<FEWBIT_F32, FEWBIT_TANH> {
 
 template <int DT>
 struct Act<DT, FEWBIT_RELU> {
-  // +0 for every x <= 0, NaN kept
-  __device__ static float f(float x) { return x > 0.0f ? x : (x == x ? 0.0f : x); }
+  // +0 for every x <= 0 (-0 included); a NaN fails the compare and is kept
+  __device__ static float f(float x) { return x <= 0.0f ? 0.0f : x; }
 };
 
 // Klambauer et al. (2017): lambda and lambda * alpha
