@@ -105,9 +105,6 @@
 #ifndef FEWBIT_NT_STORES
 #define FEWBIT_NT_STORES 1            // non-temporal stream stores
 #endif
-#ifndef FEWBIT_NT_CODE_LOADS
-#define FEWBIT_NT_CODE_LOADS 0        // code-word loads of the backward
-#endif
 
 namespace {
 
@@ -136,17 +133,6 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 // dropped store.  Cache-policy bits: 2 = nt (streaming, not kept in cache).
 constexpr int kLoadPolicy = FEWBIT_NT_LOADS ? 2 : 0;
 constexpr int kStorePolicy = FEWBIT_NT_STORES ? 2 : 0;
-// The backward reads the packed code words with the default policy, not
-// the streaming hint: measured 2-3 points faster for the 16-bit backward at
-// 1 and 2 bits (~0.5 at 3 bits) and 2-5 points for the fp32 backward.  At 1
-// and 3 bits a tile's code span (64 or 192 bytes) shares a 128-byte line
-// with its neighbour's, whose tile runs on another XCD.  The 16-bit backward
-// at 4 bits, whose spans are whole lines, is ~0.5 points faster with the
-// hint and keeps it.
-template <bool HALF, int BITS>
-constexpr int code_load_policy() {
-  return (FEWBIT_NT_CODE_LOADS || (HALF && BITS == 4)) ? 2 : 0;
-}
 
 struct Span {
   __amdgpu_buffer_rsrc_t r;
@@ -159,9 +145,8 @@ struct Span {
   __device__ void st16(uint32_t off, u32x4_t v) const {
     __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, kStorePolicy);
   }
-  template <int POLICY>
-  __device__ uint32_t ld4(uint32_t off) const {        // code words
-    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, POLICY);
+  __device__ uint32_t ld4(uint32_t off) const {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kLoadPolicy);
   }
   __device__ void st4(uint32_t off, uint32_t v) const {
     __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, kStorePolicy);
@@ -544,10 +529,7 @@ __device__ inline uint32_t quad_read(uint32_t v) {
 
 // word i of a code span
 __device__ inline void st_word(const Span& c, int i, uint32_t v) { c.st4(static_cast<uint32_t>(i) * 4u, v); }
-template <int POLICY>
-__device__ inline uint32_t ld_word(const Span& c, int i) {
-  return c.ld4<POLICY>(static_cast<uint32_t>(i) * 4u);
-}
+__device__ inline uint32_t ld_word(const Span& c, int i) { return c.ld4(static_cast<uint32_t>(i) * 4u); }
 
 // Lane field F holds the 8 codes of the lane (8*BITS bits, code j at bit
 // BITS*j).  The tile's stream is the lane fields laid end to end, so lane l's
@@ -587,17 +569,16 @@ __device__ inline void pack_store(const Span& out, uint32_t F, int lane, int64_t
 // 64 lanes together.
 template <int BITS>
 __device__ inline uint32_t load_field(const Span& base, int lane, int64_t valid) {
-  constexpr int kPol = code_load_policy<true, BITS>();
   if constexpr (BITS == 3) {
     const int k = lane & 3;
     const int widx = 3 * (lane >> 2) + k;
-    const uint32_t w = (k < 3 && widx < valid) ? ld_word<kPol>(base, widx) : 0u;
+    const uint32_t w = (k < 3 && widx < valid) ? ld_word(base, widx) : 0u;
     const uint32_t prev = quad_read<quad_perm(0, 0, 1, 2)>(w);   // word k-1 (k = 0: word 0)
     const uint32_t own = quad_read<quad_perm(0, 1, 2, 2)>(w);    // word k (k = 3: word 2)
     return __builtin_amdgcn_alignbit(own, prev, (24 * k) & 31);
   } else {
     const int widx = (8 * BITS * lane) >> 5;
-    const uint32_t v = (widx < valid) ? ld_word<kPol>(base, widx) : 0u;
+    const uint32_t v = (widx < valid) ? ld_word(base, widx) : 0u;
     return v >> ((8 * BITS * lane) & 31);
   }
 }
@@ -630,15 +611,14 @@ __device__ inline void pack_store_full(const Span& out, uint32_t F, int lane) {
 
 template <int BITS>
 __device__ inline uint32_t load_field_full(const Span& base, int lane) {
-  constexpr int kPol = code_load_policy<true, BITS>();
   if constexpr (BITS == 3) {
     const int k = lane & 3;
-    const uint32_t w = ld_word<kPol>(base, 3 * (lane >> 2) + min(k, 2));
+    const uint32_t w = ld_word(base, 3 * (lane >> 2) + min(k, 2));
     const uint32_t prev = quad_read<quad_perm(0, 0, 1, 2)>(w);   // word k-1 (k = 0: word 0)
     const uint32_t own = quad_read<quad_perm(0, 1, 2, 2)>(w);    // word k (k = 3: word 2)
     return __builtin_amdgcn_alignbit(own, prev, (24 * k) & 31);
   } else {
-    return ld_word<kPol>(base, (8 * BITS * lane) >> 5) >> ((8 * BITS * lane) & 31);
+    return ld_word(base, (8 * BITS * lane) >> 5) >> ((8 * BITS * lane) & 31);
   }
 }
 
@@ -953,9 +933,8 @@ __device__ inline uint32_t load_field32(const Span& base, int v, int lane, int64
   const int b0 = lane * C::FB;
   const int i0 = v * C::kHalfWords + (b0 >> 5);
   const int i1 = min(i0 + 1, C::kWords - 1);           // unused unless the field straddles
-  constexpr int kPol = code_load_policy<false, BITS>();
-  const uint32_t lo = (FULL || i0 < valid) ? ld_word<kPol>(base, i0) : 0u;
-  const uint32_t hi = (FULL || i1 < valid) ? ld_word<kPol>(base, i1) : 0u;
+  const uint32_t lo = (FULL || i0 < valid) ? ld_word(base, i0) : 0u;
+  const uint32_t hi = (FULL || i1 < valid) ? ld_word(base, i1) : 0u;
   return __builtin_amdgcn_alignbit(hi, lo, b0 & 31) & C::kMask;
 }
 
