@@ -64,11 +64,14 @@
  *       boundaries taken as the grid prefix plus the partial cell by the
  *       same 8-point rule.
  *
- * Parity status: activations, fit, classify, pack/unpack and backward are
- * pinned by the CPU tests (closed forms, central differences, the paper's
- * Table 1, Lloyd-Max tables, brute force, hand-made bit vectors, exhaustive
- * or sampled conversions against other libraries).  The fp32 value of y is
- * compared to the GPU within a tolerance only.
+ * Parity status: activations, weights, fit, classify, pack/unpack and
+ * backward are pinned by the CPU tests (closed forms, central differences,
+ * the paper's Table 1, Lloyd-Max tables, brute force, hand-made bit vectors,
+ * exhaustive or sampled conversions against other libraries).  The weight
+ * functions are pinned by the normal cdf and the moments of truncated
+ * normals, SELU's f by the self-normalising property its constants are
+ * defined by.  The fp32 value of y is compared to the GPU within a
+ * tolerance only.
  */
 #include <math.h>
 #include <stdint.h>
