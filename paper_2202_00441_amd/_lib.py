@@ -201,23 +201,58 @@ def _stream(dev) -> int:
     return torch.cuda.current_stream(dev).cuda_stream
 
 
+def _check_like(name: str, t, ref, n: int) -> None:
+    """t must be a contiguous device tensor on ref's device with ref's dtype
+    and n elements (an output the caller passes in)."""
+    if not t.is_cuda or t.device != ref.device:
+        raise ValueError(f"{name} must be a device tensor on {ref.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.dtype != ref.dtype:
+        raise ValueError(f"{name} must have dtype {ref.dtype}, not {t.dtype}")
+    if t.numel() != n:
+        raise ValueError(f"{name} must have {n} elements, not {t.numel()}")
+
+
+def _check_codes(codes, ref, n: int, bits: int) -> None:
+    """codes must be a contiguous device tensor of 4-byte words on ref's
+    device holding at least packed_words(n, bits) words."""
+    if not codes.is_cuda or codes.device != ref.device:
+        raise ValueError(f"codes must be a device tensor on {ref.device}")
+    if not codes.is_contiguous():
+        raise ValueError("codes must be contiguous")
+    if codes.element_size() != 4 or codes.is_floating_point():
+        raise ValueError(f"codes must hold 4-byte integer words, not {codes.dtype}")
+    need = packed_words(n, bits)
+    if codes.numel() < need:
+        raise ValueError(f"codes holds {codes.numel()} words, {need} are needed")
+
+
 def fwd(table: Table, x, y=None, codes=None):
     """y = f(x) and the packed interval indices (Listing 1, forward).
 
     x: contiguous CUDA tensor (fp32 / fp16 / bf16).  Returns (y, codes) with
     codes a uint32-sized int32 tensor of packed_words(x.numel(), bits) words.
+    y and codes may be passed in; they are checked (device, layout, dtype,
+    size) before the call, so a wrong buffer raises instead of reaching the
+    kernels.
     """
     import torch
     if not x.is_cuda or not x.is_contiguous():
         raise ValueError("x must be a contiguous device tensor")
+    dt = _dtype_code(x)
     n = x.numel()
     if y is None:
         y = torch.empty_like(x)
+    else:
+        _check_like("y", y, x, n)
     if codes is None:
         codes = torch.empty(max(packed_words(n, table.bits), 1), dtype=torch.int32,
                             device=x.device)
+    else:
+        _check_codes(codes, x, n, table.bits)
     with torch.cuda.device(x.device):
-        rc = fwd_raw(table, _dtype_code(x), x.data_ptr(), y.data_ptr(), codes.data_ptr(), n,
+        rc = fwd_raw(table, dt, x.data_ptr(), y.data_ptr(), codes.data_ptr(), n,
                      _stream(x.device))
     if rc != OK:
         raise FewbitError(rc, "fewbit_fwd")
@@ -225,15 +260,23 @@ def fwd(table: Table, x, y=None, codes=None):
 
 
 def bwd(table: Table, grad_out, codes, grad_in=None):
-    """grad_in = grad_out * v[idx] (Eq. (1) with the approximation of f')."""
+    """grad_in = grad_out * v[idx] (Eq. (1) with the approximation of f').
+
+    codes must hold at least packed_words(grad_out.numel(), bits) words on
+    grad_out's device; codes and grad_in (if passed) are checked before the
+    call."""
     import torch
     if not grad_out.is_cuda or not grad_out.is_contiguous():
         raise ValueError("grad_out must be a contiguous device tensor")
+    dt = _dtype_code(grad_out)
     n = grad_out.numel()
+    _check_codes(codes, grad_out, n, table.bits)
     if grad_in is None:
         grad_in = torch.empty_like(grad_out)
+    else:
+        _check_like("grad_in", grad_in, grad_out, n)
     with torch.cuda.device(grad_out.device):
-        rc = bwd_raw(table, _dtype_code(grad_out), grad_out.data_ptr(), codes.data_ptr(),
+        rc = bwd_raw(table, dt, grad_out.data_ptr(), codes.data_ptr(),
                      grad_in.data_ptr(), n, _stream(grad_out.device))
     if rc != OK:
         raise FewbitError(rc, "fewbit_bwd")

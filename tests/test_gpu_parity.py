@@ -325,6 +325,38 @@ def test_no_write_past_the_end(dt, bits):
         assert bool((c_full[nw:] == 0x3C3C3C3C).all()), f"codes written past the end n={n}"
 
 
+@pytest.mark.parametrize("dt,bits", [("bf16", 3), ("bf16", 4), ("f16", 3), ("f16", 4)])
+def test_no_write_past_the_end_table_kernel(dt, bits):
+    # sizes that reach the table forward, with a partial last tile, against
+    # the oracle and with canaries after every output
+    rng = np.random.default_rng(14)
+    s, v, table = _synthetic_table("gelu", bits)
+    base = P.fwd16_table_min("gelu", bits)
+    if base == NEVER:
+        pytest.skip("no table forward for this activation and bit width")
+    from parity import torch_dtype
+    for n in (base + 1, base + 37, base + 511):
+        print(f"[canary-table] {dt} b{bits} n={n}", flush=True)
+        xb = O.round_array(ODT[dt], rng.normal(0, 2, n))
+        gb = O.round_array(ODT[dt], rng.normal(0, 1, n))
+        y_ref, c_ref = O.fwd(O.GELU, ODT[dt], bits, s, xb, threads=THREADS)
+        gin_ref = O.bwd(ODT[dt], bits, v, gb, c_ref, threads=THREADS)
+        y_full, c_full = _canary_buffers(n, dt, bits)
+        gin_full, _ = _canary_buffers(n, dt, bits)
+        nw = P.packed_words(n, bits)
+        P.fwd(table, upload(xb, dt), y=y_full[:n].view(torch_dtype(dt)), codes=c_full[:nw])
+        P.bwd(table, upload(gb, dt), c_full[:nw], grad_in=gin_full[:n].view(torch_dtype(dt)))
+        torch.cuda.synchronize()
+        assert bool((y_full[n:] == 0x5A5A).all()), f"y written past the end n={n}"
+        assert bool((gin_full[n:] == 0x5A5A).all()), f"grad_in written past the end n={n}"
+        assert bool((c_full[nw:] == 0x3C3C3C3C).all()), f"codes written past the end n={n}"
+        codes = c_full[:nw].cpu().numpy().view(np.uint32)
+        assert np.array_equal(codes, c_ref), f"codes n={n}"
+        gin = gin_full[:n].cpu().numpy().view(np.uint16)
+        assert np.array_equal(gin, gin_ref), f"grad_in n={n}"
+        check_y(y_full[:n].cpu().numpy().view(np.uint16), y_ref, dt, f"y n={n}")
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_in_place(dt):
     rng = np.random.default_rng(13)
