@@ -12,6 +12,7 @@ algorithmic bytes: forward reads x (s bytes) and writes y (s) and codes
 (b/8); backward reads grad_out (s) and codes (b/8) and writes grad_in (s).
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--bits B]
+  python bench.py --all-configs                (one JSON line per workload and bit width)
   python bench.py --sweep [--sweep-n N]        (every activation x type x bits)
   python bench.py --summarize-trace DIR [--summarize-counters FETCH_DIR WRITE_DIR]
 """
@@ -101,8 +102,13 @@ ACT_NAMES = {0: "gelu", 1: "silu", 2: "sigmoid", 3: "tanh", 4: "relu", 5: "selu"
 
 def _kernel_key(name: str):
     """'fwd16_kernel<bf16,3,gelu>' style key of a library kernel named in a
-    rocprofv3 csv, or the plain name for any other kernel."""
+    rocprofv3 csv, 'ceiling_fwd<64>' style for the streaming reference
+    kernels, or the plain name for any other kernel."""
     import re
+    m = re.search(r"stream_kernel<([0-9]), ?([0-9]), ?([0-9]+), ?(true|false)>", name)
+    if m:
+        kind = {"0": "copy", "1": "fwd", "2": "bwd"}[m.group(1)]
+        return f"ceiling_{kind}<{m.group(3)}{',paired' if m.group(4) == 'true' else ''}>"
     m = re.search(r"(fwd16v_kernel|fwd16_kernel|fwd32_kernel|bwd32_kernel|bwd_kernel)<([0-9, ]+)>", name)
     if not m:
         base = name.replace("(anonymous namespace)::", "").replace("void ", "")
@@ -134,14 +140,19 @@ def _one(directory, suffix):
 def summarize_rocprof(trace_dir, fetch_dir, write_dir, workload, bits, out_traffic):
     """Print the per-kernel summary of a `rocprofv3 --kernel-trace --stats`
     run and, given the two counter runs (FETCH_SIZE, WRITE_SIZE), the HBM
-    bytes per launch of the library kernels, calibrated against the device
-    copy kernel of the same runs (which reads and writes `copy_bytes` each);
-    optionally store those bytes in profiles/traffic.json."""
+    bytes per launch of the library kernels, calibrated against the
+    benchmark's streaming copy kernel of the same runs (which reads and
+    writes `copy_bytes` each); optionally store those bytes in
+    profiles/traffic.json."""
     import workloads as WL
     w = WL.WORKLOADS[workload]
     s = 4 if w.dtype == "f32" else 2
     alg = algorithmic_bytes(w.n, w.dtype, bits)
-    copy_bytes = w.n * s
+    tiles = w.n // 512
+    # the streaming reference kernels move whole tiles only
+    ceil_bytes = {"copy": tiles * 1024 * s, "fwd": algorithmic_bytes(tiles * 512, w.dtype, bits),
+                  "bwd": algorithmic_bytes(tiles * 512, w.dtype, bits)}
+    copy_bytes = tiles * 512 * s            # the copy kernel's bytes each way
     lines = []
     if trace_dir:
         lines.append("kernel                              calls   avg_us     min_us     max_us   "
@@ -151,8 +162,8 @@ def summarize_rocprof(trace_dir, fetch_dir, write_dir, workload, bits, out_traff
             avg = float(r["AverageNs"]) / 1e3
             if key.startswith(("fwd", "bwd")):
                 b = alg
-            elif "copyBuffer" in key:
-                b = 2 * copy_bytes
+            elif key.startswith("ceiling_"):
+                b = ceil_bytes[key.split("_")[1].split("<")[0]]
             else:
                 b = None            # not a streaming kernel of this workload
             rate = (f"{b / (avg * 1e-6) / 1e9:10.1f} {b / (avg * 1e-6) / 1e9 / HBM_PEAK_GBPS:10.4f}"
@@ -169,9 +180,9 @@ def summarize_rocprof(trace_dir, fetch_dir, write_dir, workload, bits, out_traff
                 key = _kernel_key(r["Kernel_Name"])
                 per.setdefault(key, {}).setdefault(counter, []).append(
                     float(r["Counter_Value"]) * 1024.0)
-        copy = [k for k in per if "copyBuffer" in k]
+        copy = [k for k in per if k.startswith("ceiling_copy")]
         if not copy:
-            raise SystemExit("no device copy kernel in the counter runs to calibrate against")
+            raise SystemExit("no streaming copy kernel in the counter runs to calibrate against")
         cp = per[copy[0]]
         f_fetch = copy_bytes / (sum(cp["FETCH_SIZE"]) / len(cp["FETCH_SIZE"]))
         f_write = copy_bytes / (sum(cp["WRITE_SIZE"]) / len(cp["WRITE_SIZE"]))
@@ -241,7 +252,10 @@ def cpu_baseline(w, bits, x_np, g_np, seconds=10.0, chunk=1 << 22):
         return done, t_total
 
     per_elem = algorithmic_bytes(1, w.dtype, bits) * 2        # fwd + bwd bytes per element
-    threads = max(1, min(16, os.cpu_count() or 1))
+    host = host_cpu()
+    # one GPU's share of the host: the GPU machines give each GPU 16 CPUs, so the
+    # threaded oracle uses at most 16 threads whatever the host has
+    threads = max(1, min(16, host["cpus"]))
     n_mt, t_mt = run(threads, seconds)
     n_st, t_st = run(1, seconds)
     return {
@@ -249,6 +263,9 @@ def cpu_baseline(w, bits, x_np, g_np, seconds=10.0, chunk=1 << 22):
         "unit": "GB/s",
         "cores": threads,
         "kind": "oracle",
+        "host_cpus": host["cpus"],
+        "cpu_model": host["model"],
+        "threads_why": "at most 16 threads: one GPU's CPU share on this machine",
         "elements_per_s": round(n_mt / t_mt, 1),
         "single_thread": {"value": round(n_st / t_st * per_elem / 1e9, 4), "unit": "GB/s",
                           "elements_per_s": round(n_st / t_st, 1)},
@@ -256,6 +273,20 @@ def cpu_baseline(w, bits, x_np, g_np, seconds=10.0, chunk=1 << 22):
                   f"oracle in double, {threads} threads, {t_mt:.1f} s; single thread: first "
                   f"{n_st} elements, {t_st:.1f} s",
     }
+
+
+def host_cpu() -> dict:
+    """Logical CPUs of this host and their model name (/proc/cpuinfo)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpus": os.cpu_count() or 1, "model": model}
 
 
 def sweep(n: int, steps: int, warmup: int) -> None:
@@ -318,6 +349,9 @@ def main():
                     help="time forward and backward for every activation, storage type and bit "
                          "width on --sweep-n elements (one JSON line each) instead of the headline")
     ap.add_argument("--sweep-n", type=int, default=1 << 26)
+    ap.add_argument("--all-configs", action="store_true",
+                    help="every workload and bit width: back-to-back and cold kernel times, "
+                         "same-run ceilings and fit time, one JSON line each")
     ap.add_argument("--summarize-trace", metavar="DIR",
                     help="summarise a rocprofv3 --kernel-trace --stats output directory")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -363,6 +397,10 @@ def main():
         sweep(args.sweep_n, args.steps, args.warmup)
         return
 
+    if args.all_configs:
+        all_configs(args)
+        return
+
     w = WL.WORKLOADS[args.workload]
     bits = args.bits
     assert bits in w.bits, f"{w.name} runs bits {w.bits}"
@@ -373,16 +411,13 @@ def main():
     x_np, g_np = WL.inputs(w)
     print(f"[bench] generated {w.name} n={w.n} in {time.time() - t0:.1f}s", file=sys.stderr,
           flush=True)
-    view = np.int32 if w.dtype == "f32" else np.int16
-    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[w.dtype]
-    x = torch.from_numpy(x_np.view(view)).to(dev).view(tdt)
-    g = torch.from_numpy(g_np.view(view)).to(dev).view(tdt)
+    x, g = _upload(x_np, w.dtype, dev), _upload(g_np, w.dtype, dev)
     y = torch.empty_like(x)
     gin = torch.empty_like(g)
     n = w.n
     codes = torch.empty(P.packed_words(n, bits), dtype=torch.int32, device=dev)
 
-    table = P.fit_table(w.act, bits, P.Weight.from_spec(w.fit), w.fit["n_grid"])
+    table, fit_ms = fit_timed(P, w, bits)
 
     def step():
         P.fwd(table, x, y=y, codes=codes)
@@ -405,6 +440,7 @@ def main():
         ev[k][2].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
+    print(f"[bench] {args.steps} timed steps done", file=sys.stderr, flush=True)
 
     fwd_ms = [ev[k][0].elapsed_time(ev[k][1]) for k in range(args.steps)]
     bwd_ms = [ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]
@@ -414,41 +450,11 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     gbps = 2 * bytes_pass / (ms_per_step * 1e-3) / 1e9
 
-    # plain copy of the same element count (read s*n, write s*n): the
-    # practical streaming ceiling on this device
-    cp_dst = torch.empty_like(x)
-    for _ in range(3):
-        cp_dst.copy_(x)
-    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    c0.record(stream)
-    for _ in range(10):
-        cp_dst.copy_(x)
-    c1.record(stream)
-    torch.cuda.synchronize()
-    copy_ms = c0.elapsed_time(c1) / 10
-    copy_gbps = 2 * x.numel() * x.element_size() / (copy_ms * 1e-3) / 1e9
-    del cp_dst
-
-    # the same kernels cold: 1 GiB copied through the caches before each one,
-    # so that nothing of the previous pass is left in the 256 MB memory-side
-    # cache (the timed steps above run back to back, as a benchmark does)
-    fl_src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
-    fl_dst = torch.empty_like(fl_src)
-    cold = {"fwd": [], "bwd": []}
-    for _ in range(10):
-        for which in ("fwd", "bwd"):
-            fl_dst.copy_(fl_src)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            if which == "fwd":
-                P.fwd(table, x, y=y, codes=codes)
-            else:
-                P.bwd(table, g, codes, grad_in=gin)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            cold[which].append(e0.elapsed_time(e1))
-    del fl_src, fl_dst
-    cold_ms = {k: sum(v) / len(v) for k, v in cold.items()}
+    # what this device streams for the same byte mixes, same run
+    ceil = ceilings(x, y, g, gin, codes, n, bits)
+    # the same kernels cold (1 GiB copied through the caches before each)
+    cold = cold_times(P, table, x, y, g, gin, codes, reps=10)
+    print("[bench] ceilings and cold runs done", file=sys.stderr, flush=True)
 
     dom = "fwd" if fwd_avg >= bwd_avg else "bwd"
     dom_ms = fwd_avg if dom == "fwd" else bwd_avg
@@ -472,29 +478,16 @@ def main():
         "dtype": "f32",
         "storage_dtype": w.dtype,
         "data": "synthetic (seeded numpy draws, see workloads.py)",
-        "config": {
-            "workload": f"{w.name}: {w.act.upper()} {bits}-bit {w.dtype} {list(w.shape)}",
-            "act": w.act, "bits": bits, "shape": list(w.shape), "n": n,
-            "x": {"normal": f"N(0,{w.x_scale}^2)",
-                  "mixture": f"0.99 N(0,{w.x_scale}^2) + 0.01 N(0,{10 * w.x_scale}^2)",
-                  "uniform": f"U(-{w.x_scale},{w.x_scale})"}[w.x_dist],
-            "grad_out": f"N(0,{w.g_sigma}^2)",
-            "table": f"fewbit_fit_table {w.fit}",
-        },
+        "config": config_of(w, bits),
         "pct_hbm_peak": round(100 * gbps / HBM_PEAK_GBPS, 2),
         "elements_per_s": round(2 * n / (ms_per_step * 1e-3), 1),
-        "fwd": {"ms": round(fwd_avg, 5), "GB/s": round(bytes_pass / (fwd_avg * 1e-3) / 1e9, 2),
-                "elements_per_s": round(n / (fwd_avg * 1e-3), 1),
-                "frac_peak": round(bytes_pass / (fwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
-        "bwd": {"ms": round(bwd_avg, 5), "GB/s": round(bytes_pass / (bwd_avg * 1e-3) / 1e9, 2),
-                "elements_per_s": round(n / (bwd_avg * 1e-3), 1),
-                "frac_peak": round(bytes_pass / (bwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
-        "cold": {k: {"ms": round(cold_ms[k], 5),
-                     "frac_peak": round(bytes_pass / (cold_ms[k] * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
-                 for k in ("fwd", "bwd")} | {
-            "what": "each kernel alone after 1 GiB copied through the caches (10 runs, outside the timed steps)"},
-        "copy_ceiling": {"GB/s": round(copy_gbps, 2), "ms": round(copy_ms, 5),
-                         "what": "torch copy_ of x (read+write, same element count)"},
+        "fwd": kernel_record(fwd_ms, bytes_pass, n, ceil["fwd"]),
+        "bwd": kernel_record(bwd_ms, bytes_pass, n, ceil["bwd"]),
+        "cold": {k: stats_record(v, bytes_pass) for k, v in cold.items()} | {
+            "what": "each kernel alone after 1 GiB copied through the caches (10 runs, outside "
+                    "the timed steps)"},
+        "ceiling": ceil,
+        "fit_ms": fit_ms,
         "roofline": {
             "kernel": kernel_name(dom, w.dtype, bits, w.act, n, P.fwd16_table_min(w.act, bits)),
             "bound": "hbm",
@@ -505,6 +498,8 @@ def main():
             "traffic": traffic,
             "bytes_per_launch": bytes_pass,
             "avg_launch_ms": round(dom_ms, 5),
+            "ceiling_GB/s": ceil[dom]["GB/s"],
+            "frac_of_ceiling": round(achieved / ceil[dom]["GB/s"], 4),
         },
         "cpu_baseline": None,
         # context only, not a target: the memory the method saves, as the
@@ -523,6 +518,175 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, bits, x_np, g_np, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+# ---------------------------------------------------------------- timing helpers
+def _upload(a, dtype: str, dev):
+    import numpy as np
+    import torch
+    view = np.int32 if dtype == "f32" else np.int16
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dtype]
+    return torch.from_numpy(a.view(view)).to(dev).view(tdt)
+
+
+def config_of(w, bits: int) -> dict:
+    return {
+        "workload": f"{w.name}: {w.act.upper()} {bits}-bit {w.dtype} {list(w.shape)}",
+        "act": w.act, "bits": bits, "shape": list(w.shape), "n": w.n,
+        "x": {"normal": f"N(0,{w.x_scale}^2)",
+              "mixture": f"0.99 N(0,{w.x_scale}^2) + 0.01 N(0,{10 * w.x_scale}^2)",
+              "uniform": f"U(-{w.x_scale},{w.x_scale})"}[w.x_dist],
+        "grad_out": f"N(0,{w.g_sigma}^2)",
+        "table": f"fewbit_fit_table {w.fit}",
+    }
+
+
+def fit_timed(P, w, bits: int, reps: int = 3):
+    """The workload's table from the host fit (Sec. 3, done once per
+    activation), and the fit's wall time in ms over `reps` fits."""
+    ts, table = [], None
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        table = P.fit_table(w.act, bits, P.Weight.from_spec(w.fit), w.fit["n_grid"])
+        ts.append((time.perf_counter() - t0) * 1e3)
+    return table, {"min": round(min(ts), 3), "mean": round(sum(ts) / len(ts), 3),
+                   "n_grid": w.fit["n_grid"], "reps": reps}
+
+
+def stats_record(ms, bytes_pass: float) -> dict:
+    import statistics
+    med = statistics.median(ms)
+    return {"ms": round(sum(ms) / len(ms), 5), "median_ms": round(med, 5),
+            "min_ms": round(min(ms), 5),
+            "frac_peak": round(bytes_pass / (sum(ms) / len(ms) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "frac_peak_median": round(bytes_pass / (med * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
+
+
+def kernel_record(ms, bytes_pass: float, n: int, ceil) -> dict:
+    avg = sum(ms) / len(ms)
+    rec = {"GB/s": round(bytes_pass / (avg * 1e-3) / 1e9, 2),
+           "elements_per_s": round(n / (avg * 1e-3), 1)} | stats_record(ms, bytes_pass)
+    if ceil:
+        rec["frac_of_ceiling"] = round(bytes_pass / (avg * 1e-3) / 1e9 / ceil["GB/s"], 4)
+    return rec
+
+
+def _events(stream, fn, reps: int):
+    """Per-launch ms of `reps` back-to-back launches of fn on `stream`."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    return [e0.elapsed_time(e1) for e0, e1 in ev]
+
+
+def ceilings(x, y, g, gin, codes, n: int, bits: int, reps: int = 20) -> dict:
+    """Rate of the streaming reference kernels (ceiling/ceiling.hip) on the
+    workload's own buffers: a copy of x, the forward's byte mix (read x,
+    write y and the codes) and the backward's (read grad_out and the codes,
+    write grad_in), each over the whole 512-element tiles, in its fastest
+    launch shape (one wave per tile: 64 or 256 threads per workgroup in tile
+    order, or 64 threads with tiles 2p and 2p+1 on one XCD) by the median of
+    `reps` back-to-back launches."""
+    import torch
+    import ceiling as CL
+    stream = torch.cuda.current_stream()
+    tiles = n // 512
+    out = {}
+    for kind, src, dst in (("copy", x, y), ("fwd", x, y), ("bwd", g, gin)):
+        b = tiles * CL.tile_bytes(kind, src.element_size(), bits)
+        best = None
+        for shape in CL.SHAPES:
+            def fn(kind=kind, shape=shape, src=src, dst=dst):
+                CL.stream(kind, shape, src, dst, None if kind == "copy" else codes, tiles, bits)
+            for _ in range(3):
+                fn()
+            rec = stats_record(_events(stream, fn, reps), b)
+            rec = {"GB/s": round(b / (rec["median_ms"] * 1e-3) / 1e9, 2),
+                   "shape": {64: "64 threads", 256: "256 threads", 65: "64 threads, paired"}[shape],
+                   "bytes": b} | rec
+            if best is None or rec["median_ms"] < best["median_ms"]:
+                best = rec
+        out[kind] = best
+    out["what"] = ("streaming reference kernels moving the same bytes (16-byte non-temporal "
+                   "buffer accesses, one wave per 512-element tile); GB/s by the median launch")
+    return out
+
+
+def cold_times(P, table, x, y, g, gin, codes, reps: int = 10) -> dict:
+    """Each pass alone after 1 GiB has been copied through the caches, so
+    nothing of the previous pass is left in the 256 MB memory-side cache."""
+    import torch
+    dev = x.device
+    stream = torch.cuda.current_stream()
+    fl_src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    fl_dst = torch.empty_like(fl_src)
+    cold = {"fwd": [], "bwd": []}
+    for _ in range(reps):
+        for which in ("fwd", "bwd"):
+            fl_dst.copy_(fl_src)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if which == "fwd":
+                P.fwd(table, x, y=y, codes=codes)
+            else:
+                P.bwd(table, g, codes, grad_in=gin)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            cold[which].append(e0.elapsed_time(e1))
+    del fl_src, fl_dst
+    return cold
+
+
+def all_configs(args) -> None:
+    """Every workload and bit width: back-to-back and cold per-kernel times,
+    the same-run ceilings for its byte mixes and the fit time; one JSON line
+    each.  The small workloads fit in the memory-side cache, so their cold
+    figures are the ones that count."""
+    import torch
+    import workloads as WL
+    import paper_2202_00441_amd as P
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    for name, w in WL.WORKLOADS.items():
+        x_np, g_np = WL.inputs(w)
+        x, g = _upload(x_np, w.dtype, dev), _upload(g_np, w.dtype, dev)
+        del x_np, g_np
+        y, gin = torch.empty_like(x), torch.empty_like(g)
+        for bits in w.bits:
+            codes = torch.empty(P.packed_words(w.n, bits), dtype=torch.int32, device=dev)
+            table, fit_ms = fit_timed(P, w, bits)
+            for _ in range(args.warmup):
+                P.fwd(table, x, y=y, codes=codes)
+                P.bwd(table, g, codes, grad_in=gin)
+            fwd = _events(stream, lambda: P.fwd(table, x, y=y, codes=codes), args.steps)
+            bwd = _events(stream, lambda: P.bwd(table, g, codes, grad_in=gin), args.steps)
+            b = algorithmic_bytes(w.n, w.dtype, bits)
+            ceil = ceilings(x, y, g, gin, codes, w.n, bits)
+            cold = cold_times(P, table, x, y, g, gin, codes, reps=10)
+            tm = P.fwd16_table_min(w.act, bits)
+            print(json.dumps({
+                "config": config_of(w, bits), "storage_dtype": w.dtype,
+                "bytes_per_pass": b,
+                "fwd_kernel": kernel_name("fwd", w.dtype, bits, w.act, w.n, tm),
+                "bwd_kernel": kernel_name("bwd", w.dtype, bits, w.act, w.n, tm),
+                "fwd": kernel_record(fwd, b, w.n, ceil["fwd"]),
+                "bwd": kernel_record(bwd, b, w.n, ceil["bwd"]),
+                "cold": {"fwd": kernel_record(cold["fwd"], b, w.n, None),
+                         "bwd": kernel_record(cold["bwd"], b, w.n, None),
+                         "step_frac_peak": round(2 * b / ((sum(cold["fwd"]) + sum(cold["bwd"]))
+                                                          / len(cold["fwd"]) * 1e-3) / 1e9
+                                                 / HBM_PEAK_GBPS, 4)},
+                "ceiling": ceil, "fit_ms": fit_ms,
+            }), flush=True)
+            del codes
+        del x, g, y, gin
+        torch.cuda.empty_cache()
 
 
 if __name__ == "__main__":

@@ -84,15 +84,6 @@
 #ifndef FEWBIT_FWD32_UNROLL
 #define FEWBIT_FWD32_UNROLL 1
 #endif
-#ifndef FEWBIT_BWD_THREADS
-#define FEWBIT_BWD_THREADS 64
-#endif
-#ifndef FEWBIT_BWD_WG_PER_CU
-#define FEWBIT_BWD_WG_PER_CU 0
-#endif
-#ifndef FEWBIT_BWD_UNROLL
-#define FEWBIT_BWD_UNROLL 1
-#endif
 #ifndef FEWBIT_BWD32_THREADS
 #define FEWBIT_BWD32_THREADS 256
 #endif
@@ -1024,18 +1015,20 @@ __global__ __launch_bounds__(FEWBIT_FWD32_THREADS) void fwd32_kernel(
 template <int BITS>
 struct Values {
   int lane_value;
-  __device__ explicit Values(const TableArgs& tab, int lane) {
-    // v[lane mod K] by a chain of selects over scalar registers.  The values
-    // pass an empty asm barrier first, which keeps them in scalar registers:
-    // otherwise the compiler folds the chain into a per-lane load from the
-    // kernel-argument block, a vector memory load whose wait would hold back
-    // the stream loads.
+  __device__ explicit Values(const TableArgs& tab) {
+    // lane c < K holds v[c] (a chain of selects over scalar registers); the
+    // permutes read no other lane.  The values pass an empty asm barrier
+    // first, which keeps them in scalar registers: otherwise the compiler
+    // may turn the chain into a per-lane load from the kernel-argument
+    // block, a vector memory load whose wait would hold back the stream
+    // loads.
+    const int lane = static_cast<int>(threadIdx.x & (kWave - 1));
     float v = 0.0f;
 #pragma unroll
     for (int c = 0; c < (1 << BITS); ++c) {
       float t = tab.v[c];
       asm("" : "+s"(t));
-      v = ((lane & ((1 << BITS) - 1)) == c) ? t : v;
+      v = lane == c ? t : v;
     }
     lane_value = __float_as_int(v);
   }
@@ -1059,42 +1052,74 @@ __device__ inline u32x4_t grad16_tile(u32x4_t g, uint32_t F, const Values<BITS>&
   return out;
 }
 
+// The 16-bit backward runs one-wave workgroups, one tile each.  At 1 and 3
+// bits a tile's code span (64 or 192 bytes) is not a whole number of 128-byte
+// lines: tiles 2p and 2p+1 share one line.  Read by waves on different XCDs,
+// whose L2 caches are separate, that line would be fetched from memory twice
+// (a third of the code stream again at 3 bits).  So workgroup u takes tile
+// tile_of_unit(u): within each run of 16 workgroups, workgroups r and r + 8
+// take the two tiles of pair r.  The dispatcher hands workgroups to the 8
+// XCDs in turn, so the two land on the same XCD, one after the other, and the
+// shared line is fetched once.  The grid is a whole number of such runs;
+// units whose tile lies past the end do nothing.
+template <int BITS>
+struct BwdOrder {
+  static constexpr bool kPaired = BITS == 1 || BITS == 3;
+  static constexpr int64_t kRun = kPaired ? 16 : 1;
+  __host__ __device__ static int64_t tile_of_unit(int64_t u) {
+    if constexpr (kPaired) {
+      const int64_t r = u & 15;
+      return (u - r) + 2 * (r & 7) + (r >> 3);
+    } else {
+      return u;
+    }
+  }
+  // the inverse: the unit that takes tile t
+  __host__ __device__ static int64_t unit_of_tile(int64_t t) {
+    if constexpr (kPaired) {
+      const int64_t q = t & 15;
+      return (t - q) + 8 * (q & 1) + (q >> 1);
+    } else {
+      return t;
+    }
+  }
+};
+
 template <int DT, int BITS>
-__global__ __launch_bounds__(FEWBIT_BWD_THREADS) void bwd_kernel(
+__device__ inline void bwd16_full_tile(const uint16_t* g, const uint32_t* codes, uint16_t* gin,
+                                       int64_t t, int lane, const TableArgs& tab) {
+  constexpr int kWords = 16 * BITS;
+  const uint32_t lane_b = static_cast<uint32_t>(lane) * kLaneBytes;
+  const u32x4_t in = Span(g + t * kTile, kSpanBytes).ld16(lane_b);
+  const uint32_t F = load_field_full<BITS>(Span(codes + t * kWords, kWords * 4), lane);
+  // the stream loads are in flight before the values are put in place
+  __builtin_amdgcn_sched_barrier(0);
+  const Values<BITS> val(tab);
+  Span(gin + t * kTile, kSpanBytes).st16(lane_b, grad16_tile<DT, BITS>(in, F, val));
+}
+
+template <int DT, int BITS>
+__global__ __launch_bounds__(kWave) void bwd_kernel(
     const uint16_t* g, const uint32_t* __restrict__ codes, uint16_t* gin, int64_t n,
     int64_t nwords, TableArgs tab) {
-  constexpr int U = FEWBIT_BWD_UNROLL;
   constexpr int kWords = 16 * BITS;
   constexpr uint32_t kMask = (1u << BITS) - 1u;
-  const WaveIndex wi = wave_index<FEWBIT_BWD_THREADS>();
-  const Values<BITS> val(tab, wi.lane);
+  constexpr int64_t kRun = BwdOrder<BITS>::kRun;
+  const WaveIndex wi = wave_index<kWave>();
   const int64_t full = n / kTile;
-  const int64_t groups = full / U;
-  const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
-  const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
+  const int64_t units = (full + kRun - 1) / kRun * kRun;
 
-  for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
-    const int64_t t0 = gi * U;
-    u32x4_t in[U];
-    uint32_t F[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      in[u] = Span(g + (t0 + u) * kTile, kSpanBytes).ld16(lane_b);
-      F[u] = load_field_full<BITS>(Span(codes + (t0 + u) * kWords, kWords * 4), wi.lane);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      Span(gin + (t0 + u) * kTile, kSpanBytes).st16(lane_b, grad16_tile<DT, BITS>(in[u], F[u], val));
+  // one unit per wave unless the grid was capped (see grid_for)
+  for (int64_t u = wi.wave; u < units; u += wi.nwaves) {
+    const int64_t t = BwdOrder<BITS>::tile_of_unit(u);
+    if (t < full) bwd16_full_tile<DT, BITS>(g, codes, gin, t, wi.lane, tab);
   }
-  for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
-    const u32x4_t in = Span(g + t * kTile, kSpanBytes).ld16(lane_b);
-    const uint32_t F = load_field_full<BITS>(Span(codes + t * kWords, kWords * 4), wi.lane);
-    Span(gin + t * kTile, kSpanBytes).st16(lane_b, grad16_tile<DT, BITS>(in, F, val));
-  }
-  // the partial tile at the end, if any, goes to the wave that would own it
-  if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
+  // the partial tile at the end, if any, goes to the wave of its unit
+  if (n % kTile != 0 && wi.wave == BwdOrder<BITS>::unit_of_tile(full) % wi.nwaves) {
+    const Values<BITS> val(tab);
     const int64_t t = full;
     const int64_t wbase = t * kWords;
+    const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
     const uint32_t F = load_field<BITS>(Span(codes + wbase, kWords * 4), wi.lane, nwords - wbase);
     float v[kPerLane];
 #pragma unroll
@@ -1126,7 +1151,7 @@ __global__ __launch_bounds__(FEWBIT_BWD32_THREADS) void bwd32_kernel(
   constexpr int kWords = Codes32<BITS>::kWords;
   constexpr uint32_t kMask = (1u << BITS) - 1u;
   const WaveIndex wi = wave_index<FEWBIT_BWD32_THREADS>();
-  const Values<BITS> val(tab, wi.lane);
+  const Values<BITS> val(tab);
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * 4;
@@ -1361,13 +1386,18 @@ void launch_bwd(const Launch& L) {
   const int64_t nw = fewbit_packed_words(L.n, BITS);
   (void)hipGetLastError();
   if constexpr (DT == FEWBIT_F32) {
-    const dim3 grid = grid_for(L.n, FEWBIT_BWD32_THREADS / kWave, FEWBIT_BWD_WG_PER_CU, FEWBIT_BWD32_UNROLL);
+    const dim3 grid = grid_for(L.n, FEWBIT_BWD32_THREADS / kWave, 0, FEWBIT_BWD32_UNROLL);
     hipLaunchKernelGGL((bwd32_kernel<BITS>), grid, dim3(FEWBIT_BWD32_THREADS), 0, L.s,
                        static_cast<const float*>(L.in), L.codes, static_cast<float*>(L.out), L.n,
                        nw, table_args(L.t));
   } else {
-    const dim3 grid = grid_for(L.n, FEWBIT_BWD_THREADS / kWave, FEWBIT_BWD_WG_PER_CU, FEWBIT_BWD_UNROLL);
-    hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(FEWBIT_BWD_THREADS), 0, L.s,
+    // one-wave workgroups: a whole number of runs of the tile order over the
+    // full tiles, and one more workgroup when the partial tile's unit lies past them
+    const int64_t full = L.n / kTile, run = BwdOrder<BITS>::kRun;
+    int64_t units = (full + run - 1) / run * run;
+    if (L.n % kTile != 0 && units <= BwdOrder<BITS>::unit_of_tile(full)) units = BwdOrder<BITS>::unit_of_tile(full) + 1;
+    const dim3 grid = grid_for(units * kTile, 1, 0, 1);
+    hipLaunchKernelGGL((bwd_kernel<DT, BITS>), grid, dim3(kWave), 0, L.s,
                        static_cast<const uint16_t*>(L.in), L.codes, static_cast<uint16_t*>(L.out),
                        L.n, nw, table_args(L.t));
   }

@@ -36,3 +36,50 @@ def test_committed_traffic_figures():
     assert bench.measured_traffic("gelu_bf16_lm_ffn_16x2048x8192", 3, "fwd") is not None
     for key, v in rec["launches"].items():
         assert 0.99 < v["hbm_bytes"] / v["algorithmic_bytes"] < 1.1, key
+
+
+def test_ceiling_kernels_move_the_passes_bytes():
+    # the streaming reference kernels move exactly the algorithmic bytes of
+    # a pass per 512-element tile
+    import ceiling as CL
+    for dtype, s in (("bf16", 2), ("f16", 2), ("f32", 4)):
+        for bits in (1, 2, 3, 4):
+            per_tile = bench.algorithmic_bytes(512, dtype, bits)
+            assert CL.tile_bytes("fwd", s, bits) == per_tile
+            assert CL.tile_bytes("bwd", s, bits) == per_tile
+        assert CL.tile_bytes("copy", s, 3) == 2 * 512 * s
+
+
+def test_ceiling_rejects_bad_arguments_before_launching():
+    import ceiling as CL
+    f = CL._lib.ceiling_stream
+    assert f(0, 64, 2, 3, None, None, None, 0, None) == 0          # nothing to move
+    assert f(3, 64, 2, 3, 16, 16, 16, 1, None) == -1               # kind
+    assert f(1, 128, 2, 3, 16, 16, 16, 1, None) == -1              # launch shape
+    assert f(1, 64, 8, 3, 16, 16, 16, 1, None) == -1               # element size
+    assert f(1, 64, 2, 5, 16, 16, 16, 1, None) == -1               # bits
+    assert f(1, 64, 2, 3, 16, 16, None, 1, None) == -1             # codes missing
+    assert f(0, 64, 2, 3, None, 16, None, 1, None) == -1           # source missing
+
+
+def test_stats_record():
+    rec = bench.stats_record([2.0, 1.0, 3.0, 10.0], bytes_pass=8e9)
+    assert rec["ms"] == 4.0 and rec["median_ms"] == 2.5 and rec["min_ms"] == 1.0
+    assert abs(rec["frac_peak"] - 8e9 / 4e-3 / 1e9 / bench.HBM_PEAK_GBPS) < 1e-4
+
+
+def test_host_cpu():
+    h = bench.host_cpu()
+    assert h["cpus"] >= 1
+
+
+def test_kernel_keys_of_rocprof_names():
+    k = bench._kernel_key
+    assert k("void (anonymous namespace)::stream_kernel<1, 2, 64, false>(unsigned char const*, "
+             "unsigned char*, unsigned int*, long, int, unsigned int)") == "ceiling_fwd<64>"
+    assert k("void (anonymous namespace)::stream_kernel<0, 4, 256, false>(...)") == "ceiling_copy<256>"
+    assert k("void (anonymous namespace)::stream_kernel<2, 2, 64, true>(...)") == "ceiling_bwd<64,paired>"
+    assert k("void (anonymous namespace)::bwd_kernel<2, 3>(unsigned short const*, ...)") == \
+        "bwd_kernel<bf16,3>"
+    assert k("void (anonymous namespace)::fwd16_kernel<2, 3, 0>(...)") == \
+        "fwd16_kernel<bf16,3,gelu>"
