@@ -327,7 +327,8 @@ def sweep(n: int, steps: int, warmup: int) -> None:
                 b = algorithmic_bytes(n, dtype, bits)
                 print(json.dumps({
                     "act": act, "dtype": dtype, "bits": bits, "n": n,
-                    "fwd_kernel": kernel_name("fwd", dtype, bits, act, n, P.fwd16_table_min(act, bits)),
+                    "fwd_kernel": kernel_name("fwd", dtype, bits, act, n,
+                                              0 if dtype == "f32" else P.fwd16_table_min(act, bits, dtype)),
                     "fwd_ms": round(fwd_ms, 5), "fwd_frac_peak": round(b / (fwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                     "bwd_ms": round(bwd_ms, 5), "bwd_frac_peak": round(b / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                 }), flush=True)
@@ -489,7 +490,7 @@ def main():
         "ceiling": ceil,
         "fit_ms": fit_ms,
         "roofline": {
-            "kernel": kernel_name(dom, w.dtype, bits, w.act, n, P.fwd16_table_min(w.act, bits)),
+            "kernel": kernel_name(dom, w.dtype, bits, w.act, n, table_min(P, w, bits)),
             "bound": "hbm",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBPS,
@@ -527,6 +528,12 @@ def _upload(a, dtype: str, dev):
     view = np.int32 if dtype == "f32" else np.int16
     tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dtype]
     return torch.from_numpy(a.view(view)).to(dev).view(tdt)
+
+
+def table_min(P, w, bits: int) -> int:
+    """Size from which the workload's fp16 / bf16 forward runs the table
+    kernel (0 for fp32, which has none)."""
+    return 0 if w.dtype == "f32" else P.fwd16_table_min(w.act, bits, w.dtype)
 
 
 def config_of(w, bits: int) -> dict:
@@ -669,7 +676,7 @@ def all_configs(args) -> None:
             b = algorithmic_bytes(w.n, w.dtype, bits)
             ceil = ceilings(x, y, g, gin, codes, w.n, bits)
             cold = cold_times(P, table, x, y, g, gin, codes, reps=10)
-            tm = P.fwd16_table_min(w.act, bits)
+            tm = table_min(P, w, bits)
             print(json.dumps({
                 "config": config_of(w, bits), "storage_dtype": w.dtype,
                 "bytes_per_pass": b,

@@ -21,15 +21,12 @@
  *   - All argument checks run on the host before anything is launched, so a
  *     call that returns an error has written nothing.  Asynchronous device
  *     faults surface at the caller's next synchronisation.
- *   - Global state, per device: the compute-unit count (read once, it sizes
- *     the launch grid) and, for the fp16 / bf16 forward, static device
- *     tables of f over all 65536 input patterns of each activation and
- *     type (1.75 MiB of module memory).  The first fp16 / bf16 fewbit_fwd
- *     on a device with n >= fewbit_fwd16_table_min(act, bits) evaluates
- *     those tables on a private non-blocking stream and waits for that
- *     stream alone; it therefore must not be made while a stream is being
- *     captured into a graph in a mode that forbids synchronisation.  Calls
- *     are reentrant and thread-safe.
+ *   - Global state: the compute-unit count of each device, read once (it
+ *     sizes the launch grid).  The library keeps no device memory of its
+ *     own: the fp16 / bf16 forward builds its lookup tables in every
+ *     workgroup's LDS.  No call synchronises anything, so every call,
+ *     including a process's first, may be captured into a graph.  Calls are
+ *     reentrant and thread-safe.
  *   - No C++ exception crosses this interface.
  */
 #ifndef FEWBIT_H
@@ -81,6 +78,13 @@ extern "C" {
 /* Fit flag (fewbit_fit_table only; never set in a table). */
 #define FEWBIT_FLAG_REFINE    2 /* refine the DP boundaries by gradient
                                    descent on L(s, y(s)) (Sec. 3)          */
+/* Kernel choice of the fp16 / bf16 forward (may be set in a table by the
+ * caller; at most one of the two; ignored by fp32 forwards and by the
+ * backward).  Without either, fewbit_fwd picks by size (see
+ * fewbit_fwd16_table_min).  Both kernels give results within the same
+ * bounds; these flags only choose how the work is done. */
+#define FEWBIT_FLAG_TABLE_FWD   4  /* table kernel at every size           */
+#define FEWBIT_FLAG_ELEMENT_FWD 8  /* per-element kernel at every size     */
 
 typedef struct fewbit_weight {
     int32_t kind;          /* FEWBIT_W_*                                   */
@@ -104,7 +108,8 @@ typedef struct fewbit_weight {
 typedef struct fewbit_table {
     int32_t act;           /* FEWBIT_GELU .. FEWBIT_SOFTPLUS               */
     int32_t bits;          /* 1..4                                         */
-    int32_t flags;         /* 0 or FEWBIT_FLAG_SYMMETRIC                   */
+    int32_t flags;         /* FEWBIT_FLAG_SYMMETRIC, FEWBIT_FLAG_TABLE_FWD,
+                              FEWBIT_FLAG_ELEMENT_FWD                      */
     int32_t reserved;      /* must be 0                                    */
     float s[15];
     float v[16];
@@ -141,6 +146,9 @@ int fewbit_fit_table(int32_t act, int32_t bits, const fewbit_weight* w,
                      int64_t n_grid, int32_t flags, fewbit_table* out);
 
 /* Number of uint32 words holding n codes of `bits` bits: ceil(n*bits/32).
+ * This is the storage the method keeps for the backward pass instead of x:
+ * log2(k) bits per element for a k-interval approximation (Sec. 2, the
+ * compression ratio stated after Eq. (2)), packed into whole words.
  * Returns -1 for n < 0 or bits outside 1..4. */
 int64_t fewbit_packed_words(int64_t n, int32_t bits);
 
@@ -169,15 +177,19 @@ int64_t fewbit_packed_words(int64_t n, int32_t bits);
 int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, void* y,
                uint32_t* codes, int64_t n, void* stream);
 
-/* Element count from which an fp16 / bf16 forward of activation `act` at
- * `bits` bits runs the table kernel (outputs and indices looked up per input
- * bit pattern); smaller forwards evaluate f and the compares per element.
- * INT64_MAX where the per-element kernel is used at every size (ReLU at 1
- * and 2 bits, whose evaluation is cheap enough to stay bound by HBM).  Both
- * kernels give the same results; this only tells a caller (or a test) which
- * kernel a given n reaches.  Returns -1 for an unknown activation or bits
- * outside 1..4.  Host only, no device access. */
-int64_t fewbit_fwd16_table_min(int32_t act, int32_t bits);
+/* Which of the two fp16 / bf16 forward kernels fewbit_fwd runs: from the
+ * returned element count on, the table kernel (outputs and interval indices
+ * looked up per input bit pattern in tables each workgroup builds in LDS);
+ * below it, the per-element kernel (f and the compares evaluated for every
+ * element).  The count depends on the activation, the bit width and the
+ * type (dtype FEWBIT_F16 or FEWBIT_BF16); INT64_MAX where the per-element
+ * kernel runs at every size.  Both kernels give results within the same
+ * bounds: indices and codes identical, y within one unit in the last place
+ * of the correctly rounded f.  This only tells a caller (or a test) which
+ * kernel a given n reaches.  Returns -1 for an unknown activation, bits
+ * outside 1..4, or another type.  Host only, no device access.  (A query of
+ * the library's dispatch, not an operation of the paper.) */
+int64_t fewbit_fwd16_table_min(int32_t act, int32_t bits, int32_t dtype);
 
 /*
  * fewbit_bwd -- backward of the few-bit activation (Eq. (1) with f'(x)
@@ -200,7 +212,8 @@ int64_t fewbit_fwd16_table_min(int32_t act, int32_t bits);
 int fewbit_bwd(const fewbit_table* t, int32_t dtype, const void* grad_out,
                const uint32_t* codes, void* grad_in, int64_t n, void* stream);
 
-/* Static description of a status code (never NULL). */
+/* Static description of a status code (never NULL).  Error reporting of
+ * this interface, not an operation of the paper. */
 const char* fewbit_strerror(int32_t status);
 
 #ifdef __cplusplus

@@ -23,6 +23,8 @@ F32, F16, BF16 = 0, 1, 2
 W_UNIFORM, W_NORMAL, W_MIXTURE = 0, 1, 2
 FLAG_SYMMETRIC = 1
 FLAG_REFINE = 2
+FLAG_TABLE_FWD = 4        # fp16 / bf16 forward: table kernel at every size
+FLAG_ELEMENT_FWD = 8      # fp16 / bf16 forward: per-element kernel at every size
 
 ACTS = {"gelu": GELU, "silu": SILU, "swish": SILU, "sigmoid": SIGMOID, "tanh": TANH,
         "relu": RELU, "selu": SELU, "softplus": SOFTPLUS}
@@ -69,7 +71,7 @@ def _load():
     L.fewbit_bwd.restype = C.c_int
     L.fewbit_bwd.argtypes = [C.POINTER(CTable), i32, vp, vp, vp, i64, vp]
     L.fewbit_fwd16_table_min.restype = i64
-    L.fewbit_fwd16_table_min.argtypes = [i32, i32]
+    L.fewbit_fwd16_table_min.argtypes = [i32, i32, i32]
     L.fewbit_strerror.restype = C.c_char_p
     L.fewbit_strerror.argtypes = [i32]
     return L
@@ -133,6 +135,13 @@ class Table:
     def loss(self) -> float:
         return self.c.loss
 
+    def with_flags(self, flags: int) -> "Table":
+        """A copy of the table with `flags` added (e.g. a forward kernel
+        choice, FLAG_TABLE_FWD or FLAG_ELEMENT_FWD)."""
+        ct = CTable.from_buffer_copy(self.c)
+        ct.flags |= flags
+        return Table(ct)
+
     @staticmethod
     def from_values(act: int, bits: int, s: Sequence[float], v: Sequence[float],
                     flags: int = 0, loss: float = 0.0) -> "Table":
@@ -167,12 +176,13 @@ def packed_words(n: int, bits: int) -> int:
     return int(lib.fewbit_packed_words(int(n), int(bits)))
 
 
-def fwd16_table_min(act, bits: int) -> int:
-    """Element count from which fp16 / bf16 forwards of this activation and
-    bit width use the table kernel (2^63 - 1: never, the per-element kernel
-    runs at every size)."""
+def fwd16_table_min(act, bits: int, dtype="bf16") -> int:
+    """Element count from which fp16 / bf16 forwards of this activation,
+    bit width and type use the table kernel (2^63 - 1: never, the
+    per-element kernel runs at every size)."""
     a = ACTS[act] if isinstance(act, str) else int(act)
-    r = int(lib.fewbit_fwd16_table_min(a, int(bits)))
+    d = {"f16": F16, "fp16": F16, "bf16": BF16}[dtype] if isinstance(dtype, str) else int(dtype)
+    r = int(lib.fewbit_fwd16_table_min(a, int(bits), d))
     if r < 0:
         raise FewbitError(E_INVALID, "fewbit_fwd16_table_min")
     return r

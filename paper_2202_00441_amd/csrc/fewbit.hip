@@ -25,14 +25,13 @@
 // bf16 forward is persistent (see the launch-shape knobs below).
 //
 // fp16 / bf16 forward.  Output pattern and interval index are functions of
-// the 16-bit input pattern alone, so from FEWBIT_FWD16_TABLE_MIN elements on
-// each workgroup looks both up in LDS tables over all 65536 patterns: the
-// outputs (evaluated once per device by a table kernel) and the indices
-// (4 bits per pattern, built per launch from the boundaries).  A lookup
-// costs two LDS reads instead of an evaluation of f and the compares.
-// Smaller fp16 / bf16 forwards, ReLU at 1 and 2 bits (see
-// table_kernel_used), and every fp32 forward evaluate f and search the
-// boundaries per element.
+// the 16-bit input pattern alone, so from a size that depends on the type,
+// activation and bit width (kTableMinLog2) each workgroup looks both up in
+// LDS tables over all 65536 patterns, which it builds itself: the outputs
+// (mostly by rule, f where no rule holds) and the indices (4 bits per
+// pattern, from the boundaries).  A lookup costs two LDS reads instead of an
+// evaluation of f and the compares.  Smaller fp16 / bf16 forwards, and every
+// fp32 forward, evaluate f and search the boundaries per element.
 //
 // The fitted table travels as kernel arguments (scalar registers); the
 // backward spreads the values over the lanes of one register and reads
@@ -44,9 +43,9 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
-#include <mutex>
 
 #include "../../include/fewbit.h"
+#include "fwd16_rules.h"
 
 // Launch-shape knobs (compile time): threads per workgroup, workgroups per
 // CU and tiles per wave and loop trip, per kernel.  A positive WG_PER_CU
@@ -67,13 +66,9 @@
 #ifndef FEWBIT_FWD16_UNROLL
 #define FEWBIT_FWD16_UNROLL 4
 #endif
-// the fp16 / bf16 forward by evaluation (no tables): threads per workgroup,
-// and the element count from which the table kernel is used instead
+// the fp16 / bf16 forward by evaluation (no tables): threads per workgroup
 #ifndef FEWBIT_FWD16V_THREADS
 #define FEWBIT_FWD16V_THREADS 64
-#endif
-#ifndef FEWBIT_FWD16_TABLE_MIN
-#define FEWBIT_FWD16_TABLE_MIN (int64_t{1} << 22)
 #endif
 #ifndef FEWBIT_FWD32_THREADS
 #define FEWBIT_FWD32_THREADS 256
@@ -642,63 +637,103 @@ __device__ inline WaveIndex wave_index() {
 // A tile then costs two LDS reads and a few integer operations per element
 // instead of an evaluation of f and the compares.
 //
-// ylut depends only on the activation and the storage type.  All
-// (activation, 16-bit type) tables are evaluated once per device by
-// output_tables_kernel (the f of the fp32 path, then one rounding to the
-// storage type) into a static device array, before the first fp16 / bf16
-// forward on that device; each workgroup copies the one it needs into LDS
-// with direct global-to-LDS loads.  clut depends on the boundaries and is
-// built by every workgroup: the index is monotone in the pattern within one
-// sign, so each thread classifies only the two ends of its segment of
-// patterns and fills it if they agree; the few segments that hold a
-// boundary, infinities or NaNs are then classified pattern by pattern by
-// the whole wave.
-constexpr int kActs = FEWBIT_SOFTPLUS + 1;
-__device__ __attribute__((aligned(16))) uint16_t g_ytab[kActs][2][65536];
+// ylut depends only on the activation and the storage type, and most of it
+// follows a simple rule (fwd16_rules.h, written by gen_fwd16_rules.py: the
+// table is 512 blocks of 128 patterns; runs of blocks are the input itself,
+// one constant, RNE(x / 2), RNE(lambda x), or need f).  Every workgroup fills
+// its ylut from those runs, which travel as kernel arguments, and evaluates f
+// (the fp32 f of the per-element path, then one rounding) only in the blocks
+// no rule covers: for bf16 GELU 25 blocks of 512.  clut depends on the
+// boundaries and is built by every workgroup: the index is monotone in the
+// pattern within one sign, so each thread classifies only the two ends of its
+// segment of patterns and fills it if they agree; the few segments that hold
+// a boundary, infinities or NaNs are then classified pattern by pattern by the
+// whole wave.  Neither table outlives the workgroup: the library keeps no
+// device memory.
+struct OutRuns {
+  uint32_t r[fwd16_rules::kMaxRuns];
+};
 
+// ylut from the runs, by each wave on its own (no barrier, no scratch):
+//   1. wave w fills the 1 KiB chunks w, w + 8, ... of ylut (lane l the 16
+//      bytes at 16 l, so one store instruction covers consecutive banks) in
+//      the blocks whose rule is integer work on the patterns: IDENTITY,
+//      CONST and HALF (one exponent step down).  The chunks' 64 blocks are
+//      the wave's: lane l finds the run of block 4 w + 32 (l / 4) + l mod 4
+//      and the lanes of each chunk read it with one cross-lane permute.
+//      Branch-free: every lane forms both candidates and stores only in
+//      those blocks;
+//   2. the blocks of the runs that need arithmetic (EVAL: the kernel's f;
+//      SCALE), numbered in order, go to the waves in turn; 2 patterns per
+//      lane, the rule uniform over the wave.  The two steps store to
+//      different blocks.
 template <int DT, int ACT>
-__device__ void fill_output_pair(uint32_t p) {
-  reinterpret_cast<uint32_t*>(g_ytab[ACT][DT - FEWBIT_F16])[p >> 1] =
-      Half<DT>::pack(Act<DT, ACT>::f(Half<DT>::widen(p)), Act<DT, ACT>::f(Half<DT>::widen(p + 1)));
-}
-
-// One thread per pair of patterns of one of the tables.
-constexpr uint32_t kTablePairs = 2u * kActs * 32768u;
-
-template <int ACT>
-__device__ void fill_output_pair_act(uint32_t dt, uint32_t p) {
-  if (dt == 0) fill_output_pair<FEWBIT_F16, ACT>(p);
-  else fill_output_pair<FEWBIT_BF16, ACT>(p);
-}
-
-__global__ __launch_bounds__(256) void output_tables_kernel() {
-  const uint32_t gid = blockIdx.x * 256u + threadIdx.x;
-  if (gid >= kTablePairs) return;
-  const uint32_t p = (gid & 32767u) * 2u;
-  const uint32_t table = gid >> 15, dt = table & 1u;
-  switch (table >> 1) {
-    case FEWBIT_GELU: fill_output_pair_act<FEWBIT_GELU>(dt, p); break;
-    case FEWBIT_SILU: fill_output_pair_act<FEWBIT_SILU>(dt, p); break;
-    case FEWBIT_SIGMOID: fill_output_pair_act<FEWBIT_SIGMOID>(dt, p); break;
-    case FEWBIT_TANH: fill_output_pair_act<FEWBIT_TANH>(dt, p); break;
-    case FEWBIT_RELU: fill_output_pair_act<FEWBIT_RELU>(dt, p); break;
-    case FEWBIT_SELU: fill_output_pair_act<FEWBIT_SELU>(dt, p); break;
-    default: fill_output_pair_act<FEWBIT_SOFTPLUS>(dt, p); break;
+__device__ void build_output_table(uint16_t* ylut, const OutRuns& runs) {
+  using namespace fwd16_rules;
+  static_assert(FEWBIT_FWD16_THREADS == 512, "8 waves, 16 chunks each");
+  constexpr uint32_t kWaves = FEWBIT_FWD16_THREADS / kWave;
+  constexpr uint32_t kChunks = 128u / kWaves;           // 1 KiB chunks per wave
+  // x / 2 as one exponent step down (subtracted from both halves of a word)
+  constexpr uint32_t kHalfStep = DT == FEWBIT_BF16 ? 0x00800080u : 0x04000400u;
+  using H = Half<DT>;
+  uint32_t R[kMaxRuns];
+#pragma unroll
+  for (int j = 0; j < kMaxRuns; ++j) {
+    uint32_t t = runs.r[j];
+    asm("" : "+s"(t));         // keep the descriptors in scalar registers
+    R[j] = t;
   }
-}
-
-// ylut <- the device table of (ACT, DT), 1 KiB per wave instruction (lane l
-// moves bytes 16 l .. 16 l + 15 of the chunk).  The caller waits for the
-// loads and synchronises the workgroup before reading ylut.
-template <int DT, int ACT>
-__device__ void load_output_table(uint16_t* ylut) {
-  const uint8_t* src = reinterpret_cast<const uint8_t*>(g_ytab[ACT][DT - FEWBIT_F16]);
-  uint8_t* dst = reinterpret_cast<uint8_t*>(ylut);
-  const uint32_t lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  for (uint32_t c = wave; c < 128u; c += FEWBIT_FWD16_THREADS / kWave)
-    __builtin_amdgcn_global_load_lds(src + c * 1024u + lane * 16u,
-                                     (__attribute__((address_space(3))) void*)(dst + c * 1024u),
-                                     16, 0, 0);
+  const uint32_t lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  uint32_t mine = R[0];
+  {
+    const uint32_t blk = 4u * wave + 32u * (lane >> 2) + (lane & 3u);
+#pragma unroll
+    for (int j = 1; j < kMaxRuns; ++j) mine = (R[j] & 1023u) <= blk ? R[j] : mine;
+  }
+  // all permutes first: each waits in LDS order, so issuing one after the
+  // previous chunk's store would wait for that store too
+  uint32_t descs[kChunks];
+#pragma unroll
+  for (uint32_t i = 0; i < kChunks; ++i)
+    descs[i] = static_cast<uint32_t>(
+        __builtin_amdgcn_ds_bpermute(static_cast<int>(4u * (4u * i + (lane >> 4))), static_cast<int>(mine)));
+#pragma unroll
+  for (uint32_t i = 0; i < kChunks; ++i) {
+    const uint32_t p0 = (wave + kWaves * i) * 512u + lane * 8u;   // the lane's first pattern
+    const uint32_t desc = descs[i];
+    const uint32_t rule = (desc >> 12) & 15u;
+    // word e of the lane's 4: base + e step, the pattern pair (one exponent
+    // step down for HALF) or the constant
+    const uint32_t pair = (p0 | ((p0 + 1u) << 16)) - (rule == HALF ? kHalfStep : 0u);
+    // a bit select through a mask in a register: as a ?: the compiler
+    // branches around the constant's multiply
+    uint32_t is_const = rule == CONST ? ~0u : 0u;
+    asm("" : "+v"(is_const));
+    const uint32_t base = (((desc >> 16) * 0x10001u) & is_const) | (pair & ~is_const);
+    const uint32_t step = 0x00020002u & ~is_const;
+    const u32x4_t v = {base, base + step, base + 2u * step, base + 3u * step};
+    if (rule == IDENTITY || rule == CONST || rule == HALF) *reinterpret_cast<u32x4_t*>(ylut + p0) = v;
+  }
+  // the blocks needing arithmetic, numbered across the runs in order: the
+  // k-th goes to wave k mod 8
+  uint32_t* ylut32 = reinterpret_cast<uint32_t*>(ylut);
+  uint32_t before = 0;          // such blocks in the runs before run j
+#pragma unroll
+  for (int j = 0; j < kMaxRuns; ++j) {
+    const uint32_t rule = (R[j] >> 12) & 15u;
+    const uint32_t start = R[j] & 1023u;
+    const uint32_t end = j + 1 < kMaxRuns ? min(R[j + 1] & 1023u, 512u) : 512u;
+    if (start >= 512u || (rule != EVAL && rule != SCALE)) continue;
+    const uint32_t first = start + ((wave + 8u - (before & 7u)) & 7u);
+    before += end - start;
+    for (uint32_t blk = first; blk < end; blk += 8u) {
+      const uint32_t p = blk * 128u + 2u * lane;
+      const float x0 = H::widen(p), x1 = H::widen(p + 1u);
+      ylut32[blk * 64u + lane] = rule == EVAL ? H::pack(Act<DT, ACT>::f(x0), Act<DT, ACT>::f(x1))
+                                              : H::pack(x0 * kSeluLambda, x1 * kSeluLambda);
+    }
+  }
 }
 
 template <int DT, int BITS>
@@ -760,7 +795,7 @@ __device__ inline void fwd16_tile(u32x4_t in, const uint16_t* ylut, const uint8_
 template <int DT, int BITS, int ACT>
 __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
     const uint16_t* x, uint16_t* y, uint32_t* __restrict__ codes, int64_t n, int64_t nwords,
-    TableArgs tab, int symmetric) {
+    TableArgs tab, int symmetric, OutRuns runs) {
   constexpr int U = FEWBIT_FWD16_UNROLL;
   constexpr int kWords = 16 * BITS;
   // clut first: ylut's 32 KiB offset then fits the LDS instruction's
@@ -768,23 +803,32 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t tables[32768 + 2 * 65536];
   uint8_t* clut = tables;
   uint16_t* ylut = reinterpret_cast<uint16_t*>(tables + 32768);
-  load_output_table<DT, ACT>(ylut);
-  build_code_table<DT, BITS>(clut, tab, symmetric);
-  __builtin_amdgcn_s_waitcnt(0);     // the table loads have landed in LDS
-  __syncthreads();
-
   const WaveIndex wi = wave_index<FEWBIT_FWD16_THREADS>();
   const int64_t full = n / kTile;
   const int64_t groups = full / U;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
   const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
 
-  for (int64_t gi = wi.wave; gi < groups; gi += wi.nwaves) {
-    const int64_t t0 = gi * U;
-    u32x4_t in[U], out[U];
-    uint32_t F[U];
+  // the wave's first tile group is loaded before the tables are built, so
+  // its memory latency passes during the build
+  int64_t gi = wi.wave;
+  u32x4_t in[U];
+  if (gi < groups) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) in[u] = Span(x + (t0 + u) * kTile, kSpanBytes).ld16(lane_b);
+    for (int u = 0; u < U; ++u) in[u] = Span(x + (gi * U + u) * kTile, kSpanBytes).ld16(lane_b);
+  }
+  build_output_table<DT, ACT>(ylut, runs);
+  build_code_table<DT, BITS>(clut, tab, symmetric);
+  __syncthreads();
+
+  for (bool loaded = true; gi < groups; gi += wi.nwaves, loaded = false) {
+    const int64_t t0 = gi * U;
+    u32x4_t out[U];
+    uint32_t F[U];
+    if (!loaded) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) in[u] = Span(x + (t0 + u) * kTile, kSpanBytes).ld16(lane_b);
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) fwd16_tile<BITS>(in[u], ylut, clut, out[u], F[u]);
 #pragma unroll
@@ -819,12 +863,10 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
 }
 
 // fp16 / bf16 forward by evaluation: f and the compares for every element,
-// no tables.  The table kernel above needs ~3 us of setup per launch and a
-// persistent grid; below FEWBIT_FWD16_TABLE_MIN elements this kernel, one
-// wave per tile with no setup, is faster, and so it is at every size where
-// f and the classification are cheap enough to leave it bound by HBM
-// (table_kernel_used).  Outputs are the table kernel's: the tables hold this
-// same f and rounding.
+// no tables.  The table kernel above builds its tables in every workgroup
+// and runs a persistent grid; below the sizes of kTableMinLog2 this kernel,
+// one wave per tile with no setup, is faster.  Where the table kernel
+// evaluates f (the blocks no rule covers) it uses this same f and rounding.
 // y and the two codes of the element pair in word w; the codes go to bits
 // shift .. shift + 2*BITS - 1 of F.
 template <int DT, int BITS, int ACT>
@@ -1205,7 +1247,9 @@ int check_table(const fewbit_table* t) {
   if (!t) return FEWBIT_E_NULL;
   if (t->bits < 1 || t->bits > 4) return FEWBIT_E_BITS;
   if (t->act < FEWBIT_GELU || t->act > FEWBIT_SOFTPLUS) return FEWBIT_E_INVALID;
-  if ((t->flags & ~FEWBIT_FLAG_SYMMETRIC) != 0 || t->reserved != 0) return FEWBIT_E_INVALID;
+  constexpr int32_t kFlags = FEWBIT_FLAG_SYMMETRIC | FEWBIT_FLAG_TABLE_FWD | FEWBIT_FLAG_ELEMENT_FWD;
+  if ((t->flags & ~kFlags) != 0 || t->reserved != 0) return FEWBIT_E_INVALID;
+  if ((t->flags & FEWBIT_FLAG_TABLE_FWD) && (t->flags & FEWBIT_FLAG_ELEMENT_FWD)) return FEWBIT_E_INVALID;
   const int K = 1 << t->bits;
   for (int m = 0; m < K - 1; ++m) {
     if (!std::isfinite(t->s[m])) return FEWBIT_E_NUMERIC;
@@ -1264,37 +1308,6 @@ dim3 grid_for(int64_t n, int waves_per_block, int wg_per_cu, int unroll) {
   return dim3(static_cast<unsigned>(blocks));
 }
 
-// The output tables of the fp16 / bf16 forward, once per device: evaluated
-// on a private non-blocking stream that the host waits for, so that every
-// later launch on any stream reads complete tables.  Thread-safe.
-int ensure_output_tables() {
-  static std::atomic<int> ready[64];
-  static std::mutex mu;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return FEWBIT_E_HIP;
-  if (ready[dev].load(std::memory_order_acquire)) return FEWBIT_OK;
-  std::lock_guard<std::mutex> lock(mu);
-  if (ready[dev].load(std::memory_order_relaxed)) return FEWBIT_OK;
-  hipStream_t s = nullptr;
-  hipError_t e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
-  if (e == hipSuccess) {
-    (void)hipGetLastError();
-    hipLaunchKernelGGL(output_tables_kernel, dim3(kTablePairs / 256u), dim3(256), 0, s);
-    e = hipGetLastError();
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    const hipError_t d = hipStreamDestroy(s);
-    if (e == hipSuccess) e = d;
-  }
-  if (e != hipSuccess) {
-    if (std::getenv("FEWBIT_DEBUG"))
-      std::fprintf(stderr, "fewbit: output tables: %s (%s)\n", hipGetErrorName(e),
-                   hipGetErrorString(e));
-    return FEWBIT_E_HIP;
-  }
-  ready[dev].store(1, std::memory_order_release);
-  return FEWBIT_OK;
-}
-
 // The stream must belong to the current device: the grid size, the output
 // tables and the launch all refer to the current device.
 int check_stream_device(hipStream_t stream) {
@@ -1314,20 +1327,51 @@ struct Launch {
   hipStream_t s;
 };
 
-// Whether an fp16 / bf16 forward of (act, bits) uses the table kernel from
-// FEWBIT_FWD16_TABLE_MIN elements on.  ReLU at 1 or 2 bits does not: its f
-// is a select and its classification one or two compares, so the
-// per-element kernel stays bound by HBM and, as a one-wave-per-tile grid,
-// streams faster than the persistent table kernel at every size (about 79%
-// against 73% of the HBM peak at 1 bit, 76% against 73% at 2 bits).  For
-// every other activation and bit width the evaluation costs more than the
-// persistent grid does.
-constexpr bool table_kernel_used(int act, int bits) {
-  return !(act == FEWBIT_RELU && bits <= 2);
+// The output-table runs of (ACT, DT) as a kernel argument; unused entries
+// start past the last block.
+template <int DT, int ACT>
+OutRuns out_runs() {
+  const fwd16_rules::Runs& src = fwd16_rules::kRuns[ACT][DT == FEWBIT_BF16 ? 1 : 0];
+  OutRuns r;
+  for (int j = 0; j < fwd16_rules::kMaxRuns; ++j) r.r[j] = j < src.count ? src.r[j] : fwd16_rules::kUnused;
+  return r;
 }
 
-int64_t table_min_of(int act, int bits) {
-  return table_kernel_used(act, bits) ? FEWBIT_FWD16_TABLE_MIN : INT64_MAX;
+// log2 of the element count from which an fp16 / bf16 forward runs the table
+// kernel, by [type: fp16, bf16][activation][bits - 1]; 63: never.  The table
+// kernel builds its tables in every workgroup (7-10 us of fixed cost for
+// bf16, 12-15 us for fp16, whose tables need f in far more blocks) and runs
+// as a persistent grid; the per-element kernel has no setup and streams as
+// a one-wave-per-tile grid, but evaluates f and the compares per element.
+// Measured on MI355X (x ~ N(0, 3^2), 2^22 .. 2^27 elements): the table kernel
+// wins from the size given, where the evaluation costs more than the setup
+// and the persistent grid; at 1 bit (and for ReLU) the per-element kernel
+// stays ahead at every size measured, and Softplus, whose per-element f is
+// the most expensive, switches first.
+constexpr uint8_t kTableMinLog2[2][FEWBIT_SOFTPLUS + 1][4] = {
+    {   // fp16
+        {27, 26, 25, 26},   // gelu
+        {63, 27, 25, 26},   // silu
+        {63, 27, 25, 26},   // sigmoid
+        {26, 25, 24, 25},   // tanh
+        {63, 63, 63, 63},   // relu
+        {63, 27, 26, 26},   // selu
+        {23, 23, 23, 24},   // softplus
+    },
+    {   // bf16
+        {27, 26, 25, 25},   // gelu
+        {63, 27, 25, 25},   // silu
+        {63, 27, 25, 26},   // sigmoid
+        {24, 24, 24, 24},   // tanh
+        {63, 63, 26, 63},   // relu
+        {63, 27, 26, 26},   // selu
+        {21, 21, 21, 21},   // softplus
+    },
+};
+
+int64_t table_min_of(int dt, int act, int bits) {
+  const int lg = kTableMinLog2[dt == FEWBIT_BF16 ? 1 : 0][act][bits - 1];
+  return lg >= 63 ? INT64_MAX : int64_t{1} << lg;
 }
 
 template <int DT, int BITS, int ACT>
@@ -1341,19 +1385,20 @@ void launch_fwd(const Launch& L) {
                        static_cast<const float*>(L.in), static_cast<float*>(L.out), L.codes, L.n,
                        nw, table_args(L.t), sym);
   } else {
-    constexpr bool kTable = table_kernel_used(ACT, BITS);
-    if (!kTable || L.n < FEWBIT_FWD16_TABLE_MIN) {
+    const bool table = (L.t->flags & FEWBIT_FLAG_TABLE_FWD) ||
+                       (!(L.t->flags & FEWBIT_FLAG_ELEMENT_FWD) && L.n >= table_min_of(DT, ACT, BITS));
+    if (!table) {
       const dim3 grid = grid_for(L.n, FEWBIT_FWD16V_THREADS / kWave, 0, 1);
       (void)hipGetLastError();
       hipLaunchKernelGGL((fwd16v_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16V_THREADS), 0, L.s,
                          static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
                          L.n, nw, table_args(L.t), sym);
-    } else if constexpr (kTable) {
+    } else {
       const dim3 grid = grid_for(L.n, FEWBIT_FWD16_THREADS / kWave, FEWBIT_FWD16_WG_PER_CU, FEWBIT_FWD16_UNROLL);
       (void)hipGetLastError();
       hipLaunchKernelGGL((fwd16_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16_THREADS), 0, L.s,
                          static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,
-                         L.n, nw, table_args(L.t), sym);
+                         L.n, nw, table_args(L.t), sym, out_runs<DT, ACT>());
     }
   }
 }
@@ -1438,10 +1483,6 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   if (misaligned(x) || misaligned(y) || misaligned(codes)) return FEWBIT_E_ALIGN;
   rc = check_stream_device(static_cast<hipStream_t>(stream));
   if (rc != FEWBIT_OK) return rc;
-  if (dtype != FEWBIT_F32 && n >= table_min_of(t->act, t->bits)) {
-    rc = ensure_output_tables();
-    if (rc != FEWBIT_OK) return rc;
-  }
   const Launch L{t, x, y, codes, n, static_cast<hipStream_t>(stream)};
   switch (dtype) {
     case FEWBIT_F32: launch_fwd_bits<FEWBIT_F32>(L); break;
@@ -1451,9 +1492,11 @@ extern "C" int fewbit_fwd(const fewbit_table* t, int32_t dtype, const void* x, v
   return launch_status("fewbit_fwd");
 }
 
-extern "C" int64_t fewbit_fwd16_table_min(int32_t act, int32_t bits) {
-  if (act < FEWBIT_GELU || act > FEWBIT_SOFTPLUS || bits < 1 || bits > 4) return -1;
-  return table_min_of(act, bits);
+extern "C" int64_t fewbit_fwd16_table_min(int32_t act, int32_t bits, int32_t dtype) {
+  if (act < FEWBIT_GELU || act > FEWBIT_SOFTPLUS || bits < 1 || bits > 4 ||
+      (dtype != FEWBIT_F16 && dtype != FEWBIT_BF16))
+    return -1;
+  return table_min_of(dtype, act, bits);
 }
 
 extern "C" int fewbit_bwd(const fewbit_table* t, int32_t dtype, const void* grad_out,

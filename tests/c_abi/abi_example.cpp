@@ -52,13 +52,15 @@ bool write_file(const std::string& path, const void* p, size_t bytes) {
 }
 
 int run_case(const char* dir, const char* name, int32_t act, int32_t dtype, int32_t bits,
-             int32_t flags, const fewbit_weight& w, int64_t n, double scale, hipStream_t stream) {
+             int32_t flags, const fewbit_weight& w, int64_t n, double scale, hipStream_t stream,
+             int32_t kernel_flags = 0) {
   fewbit_table t;
   int rc = fewbit_fit_table(act, bits, &w, 2000, flags, &t);
   if (rc != FEWBIT_OK) {
     std::fprintf(stderr, "%s: fit: %s\n", name, fewbit_strerror(rc));
     return 1;
   }
+  t.flags |= kernel_flags;     // the forward kernel choice, if any
   const size_t esz = dtype == FEWBIT_F32 ? 4 : 2;
   std::vector<uint8_t> x(n * esz), g(n * esz);
   Lcg r{static_cast<uint64_t>(n) * 2654435761u + static_cast<uint64_t>(act)};
@@ -121,9 +123,10 @@ int main(int argc, char** argv) {
   }
   const fewbit_weight normal{FEWBIT_W_NORMAL, 0, -10.0, 10.0, 0.0, 1.0, 0.0, 1.0};
   const fewbit_weight uniform{FEWBIT_W_UNIFORM, 0, -8.0, 8.0, 0.0, 1.0, 0.0, 1.0};
-  // bf16 above the table-kernel size, on the null stream
+  // bf16 through the table kernel (chosen in the table), on the null stream
+  if (fewbit_fwd16_table_min(FEWBIT_GELU, 3, FEWBIT_BF16) <= 0) return 1;
   if (run_case(argv[1], "gelu_bf16_b3", FEWBIT_GELU, FEWBIT_BF16, 3, 0, normal,
-               fewbit_fwd16_table_min(FEWBIT_GELU, 3) + 1237, 3.0, nullptr))
+               (int64_t{1} << 22) + 1237, 3.0, nullptr, FEWBIT_FLAG_TABLE_FWD))
     return 1;
   hipStream_t s;
   HIP_OK(hipStreamCreate(&s));

@@ -112,11 +112,14 @@ def check_exact(got: np.ndarray, ref: np.ndarray, what: str):
                            f"{[hex(int(v)) for v in ref[bad[:4]]]}")
 
 
-def run_case(key: str, dt: str, x_bits: np.ndarray, g_bits: np.ndarray, label: str = ""):
-    """fwd + bwd on the GPU through the C ABI vs the oracle on the same bits."""
+def run_case(key: str, dt: str, x_bits: np.ndarray, g_bits: np.ndarray, label: str = "",
+             flags: int = 0):
+    """fwd + bwd on the GPU through the C ABI vs the oracle on the same bits
+    (flags: a forward kernel choice added to the table)."""
     import torch
     import paper_2202_00441_amd as P
     spec, table = golden_table(key)
+    table = table.with_flags(flags)
     bits = spec["bits"]
     n = x_bits.size
     print(f"[parity] {label or key} dt={dt} n={n} bits={bits}", flush=True)

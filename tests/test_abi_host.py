@@ -40,19 +40,37 @@ def test_exports_every_declared_symbol():
 
 
 def test_fwd16_table_min():
-    # a positive element count, a whole number of 512-element tiles, the
-    # same for every activation and bit width that uses the table kernel
-    m = P.fwd16_table_min("gelu", 3)
-    assert m > 0 and m % 512 == 0
-    for act in P.ACTS:
-        for bits in (1, 2, 3, 4):
-            expect = 2 ** 63 - 1 if (act == "relu" and bits <= 2) else m
-            assert P.fwd16_table_min(act, bits) == expect, (act, bits)
-    assert _lib.lib.fewbit_fwd16_table_min(7, 3) == -1
-    assert _lib.lib.fewbit_fwd16_table_min(0, 0) == -1
-    assert _lib.lib.fewbit_fwd16_table_min(0, 5) == -1
+    # a whole number of 512-element tiles, or "never"; per type, activation
+    # and bit width; -1 for bad arguments (fp32 has no table kernel)
+    never = 2 ** 63 - 1
+    for dt in ("f16", "bf16"):
+        for act in P.ACTS:
+            for bits in (1, 2, 3, 4):
+                m = P.fwd16_table_min(act, bits, dt)
+                assert m == never or (m > 0 and m % 512 == 0), (act, bits, dt)
+    assert P.fwd16_table_min("relu", 1, "bf16") == never
+    assert P.fwd16_table_min("gelu", 3, "bf16") <= 1 << 28     # the large-LM workload
+    L = _lib.lib
+    assert L.fewbit_fwd16_table_min(7, 3, P.BF16) == -1
+    assert L.fewbit_fwd16_table_min(0, 0, P.BF16) == -1
+    assert L.fewbit_fwd16_table_min(0, 5, P.BF16) == -1
+    assert L.fewbit_fwd16_table_min(0, 3, P.F32) == -1
+    assert L.fewbit_fwd16_table_min(0, 3, 3) == -1
     with pytest.raises(P.FewbitError):
         P.fwd16_table_min(-1, 3)
+
+
+def test_kernel_choice_flags():
+    # either forward kernel may be chosen in the table, not both
+    A = 16
+    for flags, ok in ((P.FLAG_TABLE_FWD, True), (P.FLAG_ELEMENT_FWD, True),
+                      (P.FLAG_TABLE_FWD | P.FLAG_ELEMENT_FWD, False)):
+        t = _table().with_flags(flags)
+        # a stream of another device would be rejected after the table check,
+        # so only the table checks are reached with n = 0 (a no-op when valid)
+        rc = _lib.lib.fewbit_fwd(C.byref(t.c), P.BF16, A, A, A, 0, None)
+        assert (rc == _lib.OK) == ok, flags
+    assert _table().with_flags(P.FLAG_TABLE_FWD).flags == P.FLAG_TABLE_FWD
 
 
 def test_packed_words():
