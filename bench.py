@@ -109,6 +109,9 @@ def _kernel_key(name: str):
     if m:
         kind = {"0": "copy", "1": "fwd", "2": "bwd"}[m.group(1)]
         return f"ceiling_{kind}<{m.group(3)}{',paired' if m.group(4) == 'true' else ''}>"
+    m = re.search(r"persist_kernel<([0-9]), ?([0-9])>", name)
+    if m:
+        return f"ceiling_{ {'0': 'copy', '1': 'fwd', '2': 'bwd'}[m.group(1)]}<persistent>"
     m = re.search(r"(fwd16v_kernel|fwd16_kernel|fwd32_kernel|bwd32_kernel|bwd_kernel)<([0-9, ]+)>", name)
     if not m:
         base = name.replace("(anonymous namespace)::", "").replace("void ", "")
@@ -516,6 +519,14 @@ def main():
             "bits": [1, 2, 3, 4],
         },
     }
+    fwd_kernel = kernel_name("fwd", w.dtype, bits, w.act, n, table_min(P, w, bits))
+    out["fwd"]["kernel"] = fwd_kernel
+    out["bwd"]["kernel"] = kernel_name("bwd", w.dtype, bits, w.act, n, table_min(P, w, bits))
+    if fwd_kernel.startswith("fwd16_kernel"):
+        # the table forward runs one persistent workgroup per CU: its rate
+        # against what that launch shape streams for the same bytes
+        out["fwd"]["frac_of_persistent_shape"] = round(
+            bytes_pass / (fwd_avg * 1e-3) / 1e9 / ceil["fwd_persistent_shape"]["GB/s"], 4)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, bits, x_np, g_np, args.cpu_seconds)
     print(json.dumps(out), flush=True)
@@ -619,8 +630,21 @@ def ceilings(x, y, g, gin, codes, n: int, bits: int, reps: int = 20) -> dict:
             if best is None or rec["median_ms"] < best["median_ms"]:
                 best = rec
         out[kind] = best
+    # the forward mix in the 16-bit table forward's own launch shape (one
+    # persistent workgroup per CU): what that shape streams, not a ceiling
+    b = tiles * CL.tile_bytes("fwd", x.element_size(), bits)
+
+    def fn():
+        CL.stream("fwd", CL.PERSISTENT, x, y, codes, tiles, bits)
+    for _ in range(3):
+        fn()
+    rec = stats_record(_events(stream, fn, reps), b)
+    out["fwd_persistent_shape"] = {"GB/s": round(b / (rec["median_ms"] * 1e-3) / 1e9, 2),
+                                   "shape": "persistent, one 512-thread workgroup per CU",
+                                   "bytes": b} | rec
     out["what"] = ("streaming reference kernels moving the same bytes (16-byte non-temporal "
-                   "buffer accesses, one wave per 512-element tile); GB/s by the median launch")
+                   "buffer accesses, one wave per 512-element tile); GB/s by the median launch; "
+                   "fwd_persistent_shape: the forward mix in the table forward's launch shape")
     return out
 
 
@@ -677,12 +701,17 @@ def all_configs(args) -> None:
             ceil = ceilings(x, y, g, gin, codes, w.n, bits)
             cold = cold_times(P, table, x, y, g, gin, codes, reps=10)
             tm = table_min(P, w, bits)
+            fk = kernel_name("fwd", w.dtype, bits, w.act, w.n, tm)
+            fwd_rec = kernel_record(fwd, b, w.n, ceil["fwd"])
+            if fk.startswith("fwd16_kernel"):
+                fwd_rec["frac_of_persistent_shape"] = round(
+                    b / (sum(fwd) / len(fwd) * 1e-3) / 1e9 / ceil["fwd_persistent_shape"]["GB/s"], 4)
             print(json.dumps({
                 "config": config_of(w, bits), "storage_dtype": w.dtype,
                 "bytes_per_pass": b,
-                "fwd_kernel": kernel_name("fwd", w.dtype, bits, w.act, w.n, tm),
+                "fwd_kernel": fk,
                 "bwd_kernel": kernel_name("bwd", w.dtype, bits, w.act, w.n, tm),
-                "fwd": kernel_record(fwd, b, w.n, ceil["fwd"]),
+                "fwd": fwd_rec,
                 "bwd": kernel_record(bwd, b, w.n, ceil["bwd"]),
                 "cold": {"fwd": kernel_record(cold["fwd"], b, w.n, None),
                          "bwd": kernel_record(cold["bwd"], b, w.n, None),

@@ -4,9 +4,11 @@ stream(kind, shape, x, y, codes, tiles, bits): moves `tiles` whole 512-element
 tiles with the byte mix of a copy ("copy"), of the few-bit forward ("fwd":
 read x, write y and the codes) or of the backward ("bwd": read grad_out and
 the codes, write grad_in), on the current stream.  Launch shapes: 64 or 256
-threads per workgroup in tile order, or 65 (64 threads, tiles 2p and 2p+1 on
-workgroups 8 apart, i.e. on one XCD).  Used only by bench.py, to
-measure in the same run what the device streams for each byte mix.
+threads per workgroup in tile order, 65 (64 threads, tiles 2p and 2p+1 on
+workgroups 8 apart, i.e. on one XCD), or PERSISTENT (512: one persistent
+512-thread workgroup per compute unit, the 16-bit table forward's launch
+shape; not a ceiling candidate).  Used only by bench.py, to measure in the
+same run what the device streams for each byte mix.
 """
 import ctypes as C
 import os
@@ -27,7 +29,8 @@ def tile_bytes(kind: str, elem_bytes: int, bits: int) -> int:
     return 2 * data + (0 if kind == "copy" else 64 * bits)
 
 
-SHAPES = (64, 256, 65)
+SHAPES = (64, 256, 65)       # the ceiling candidates
+PERSISTENT = 512
 
 
 def stream(kind: str, shape: int, src, dst, codes, tiles: int, bits: int) -> None:

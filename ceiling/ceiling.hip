@@ -22,6 +22,12 @@
 // L2 caches are separate) it is fetched twice; the paired launch shape gives
 // the two tiles to one-wave workgroups 8 apart in launch order, which the
 // dispatcher places on the same XCD, so the line is fetched once.
+//
+// One more shape stands for the 16-bit table forward's own launch: one
+// persistent 512-thread workgroup per compute unit (LDS-bound, as the
+// forward's 160 KiB of tables make it), wave w of W taking tiles w, w + W,
+// w + 2W, ... with the loads of its next four tiles in flight.  It is not a
+// candidate for the ceiling; it shows what that launch shape can stream.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -75,6 +81,73 @@ __global__ __launch_bounds__(TPB) void stream_kernel(const uint8_t* src, uint8_t
   if constexpr (KIND == 1) __builtin_amdgcn_raw_buffer_store_b32(v[0].x ^ v[0].y ^ salt, rc, wo, 0, 2);
 }
 
+// The persistent shape: per tile, the loads (data and, for the backward mix,
+// the code word) and then the stores, as in stream_kernel.
+template <int KIND, int S>
+struct Loaded {
+  u32x4_t v[S / 2];
+  uint32_t c;
+};
+template <int KIND, int S>
+__device__ inline Loaded<KIND, S> load_tile(const uint8_t* src, const uint32_t* codes, int64_t t, int64_t tiles,
+                                            int words, int lane) {
+  constexpr uint32_t kTileBytes = 512u * S;
+  const bool in = t < tiles;
+  const auto rs = span(src + (in ? t : 0) * kTileBytes, in ? kTileBytes : 0u);
+  Loaded<KIND, S> r;
+#pragma unroll
+  for (int h = 0; h < S / 2; ++h) r.v[h] = ld16(rs, h * 1024u + lane * 16u);
+  r.c = 0;
+  if constexpr (KIND == 2) {
+    const auto rc = span(codes + (in ? t : 0) * words, in ? static_cast<uint32_t>(words) * 4u : 0u);
+    r.c = __builtin_amdgcn_raw_buffer_load_b32(rc, static_cast<uint32_t>(lane % words) * 4u, 0, 2);
+  }
+  return r;
+}
+template <int KIND, int S>
+__device__ inline void store_tile(uint8_t* dst, uint32_t* codes, int64_t t, int words, int lane,
+                                  const Loaded<KIND, S>& r, uint32_t salt) {
+  constexpr uint32_t kTileBytes = 512u * S;
+  const auto rd = span(dst + t * kTileBytes, kTileBytes);
+  const uint32_t c = salt ^ r.c;
+#pragma unroll
+  for (int h = 0; h < S / 2; ++h) st16(rd, h * 1024u + lane * 16u, r.v[h] ^ c);
+  if constexpr (KIND == 1) {
+    const auto rc = span(codes + t * words, static_cast<uint32_t>(words) * 4u);
+    __builtin_amdgcn_raw_buffer_store_b32(r.v[0].x ^ r.v[0].y ^ salt, rc, static_cast<uint32_t>(lane % words) * 4u,
+                                          0, 2);
+  }
+}
+
+constexpr int kPersistThreads = 512;
+constexpr int kPersistDepth = 4;
+
+template <int KIND, int S>
+__global__ __launch_bounds__(kPersistThreads) void persist_kernel(const uint8_t* src, uint8_t* dst, uint32_t* codes,
+                                                                  int64_t tiles, int words, uint32_t salt) {
+  // 156 KiB of LDS: one workgroup per compute unit
+  __shared__ uint32_t hold[156 * 1024 / 4];
+  const int lane = threadIdx.x & 63;
+  const int64_t w = static_cast<int64_t>(blockIdx.x) * (kPersistThreads / 64) +
+                    __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / 64));
+  const int64_t nw = static_cast<int64_t>(gridDim.x) * (kPersistThreads / 64);
+  if (threadIdx.x == 0) hold[0] = salt;
+  __syncthreads();
+  const uint32_t s = hold[0];
+  Loaded<KIND, S> q[kPersistDepth];
+#pragma unroll
+  for (int d = 0; d < kPersistDepth; ++d) q[d] = load_tile<KIND, S>(src, codes, w + d * nw, tiles, words, lane);
+  for (int64_t t = w; t < tiles; t += kPersistDepth * nw) {
+#pragma unroll
+    for (int d = 0; d < kPersistDepth; ++d) {
+      const int64_t tt = t + d * nw;
+      const Loaded<KIND, S> cur = q[d];
+      q[d] = load_tile<KIND, S>(src, codes, tt + kPersistDepth * nw, tiles, words, lane);
+      if (tt < tiles) store_tile<KIND, S>(dst, codes, tt, words, lane, cur, s);
+    }
+  }
+}
+
 template <int KIND, int S>
 hipError_t launch_s(int shape, const void* src, void* dst, uint32_t* codes, int64_t tiles, int words,
                     hipStream_t s) {
@@ -94,6 +167,15 @@ hipError_t launch_s(int shape, const void* src, void* dst, uint32_t* codes, int6
       hipLaunchKernelGGL((stream_kernel<KIND, S, 64, true>), dim3(static_cast<unsigned>((tiles + 15) / 16 * 16)),
                          dim3(64), 0, s, in, out, codes, tiles, words, 0u);
       break;
+    case 512: {   // persistent: one workgroup per compute unit
+      int dev = 0, cus = 0;
+      if (hipGetDevice(&dev) != hipSuccess ||
+          hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return hipErrorInvalidValue;
+      hipLaunchKernelGGL((persist_kernel<KIND, S>), dim3(static_cast<unsigned>(cus)), dim3(kPersistThreads), 0, s,
+                         in, out, codes, tiles, words, 0u);
+      break;
+    }
     default:
       return hipErrorInvalidValue;
   }
@@ -105,14 +187,16 @@ hipError_t launch_s(int shape, const void* src, void* dst, uint32_t* codes, int6
 // Streams `tiles` whole 512-element tiles of kind 0 (copy), 1 (forward byte
 // mix) or 2 (backward byte mix) of elem_bytes-byte elements (2 or 4) with
 // bits-bit codes (1..4) on `stream`, in launch shape `shape`: 64 or 256
-// threads per workgroup in tile order, or 65: 64 threads in the paired order.
+// threads per workgroup in tile order, 65: 64 threads in the paired order,
+// or 512: persistent 512-thread workgroups, one per compute unit of the
+// current device.
 // src and dst hold tiles * 512 * elem_bytes bytes, codes tiles * 16 * bits
 // words (unused for the copy); all 16-byte aligned.  Returns 0, or -1 for an
 // argument error, -2 for a launch error.
 extern "C" int ceiling_stream(int kind, int shape, int elem_bytes, int bits, const void* src, void* dst,
                               uint32_t* codes, int64_t tiles, void* stream) {
   if (kind < 0 || kind > 2 || (elem_bytes != 2 && elem_bytes != 4) || bits < 1 || bits > 4 ||
-      tiles < 0 || tiles > (int64_t{1} << 31) - 16 || (shape != 64 && shape != 256 && shape != 65))
+      tiles < 0 || tiles > (int64_t{1} << 31) - 16 || (shape != 64 && shape != 256 && shape != 65 && shape != 512))
     return -1;
   if (tiles == 0) return 0;
   if (!src || !dst || (kind != 0 && !codes)) return -1;

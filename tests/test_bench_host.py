@@ -56,6 +56,8 @@ def test_ceiling_rejects_bad_arguments_before_launching():
     assert f(0, 64, 2, 3, None, None, None, 0, None) == 0          # nothing to move
     assert f(3, 64, 2, 3, 16, 16, 16, 1, None) == -1               # kind
     assert f(1, 128, 2, 3, 16, 16, 16, 1, None) == -1              # launch shape
+    assert f(1, 513, 2, 3, 16, 16, 16, 1, None) == -1
+    assert f(1, 512, 2, 3, None, None, None, 0, None) == 0         # persistent, nothing to move
     assert f(1, 64, 8, 3, 16, 16, 16, 1, None) == -1               # element size
     assert f(1, 64, 2, 5, 16, 16, 16, 1, None) == -1               # bits
     assert f(1, 64, 2, 3, 16, 16, None, 1, None) == -1             # codes missing
@@ -79,6 +81,7 @@ def test_kernel_keys_of_rocprof_names():
              "unsigned char*, unsigned int*, long, int, unsigned int)") == "ceiling_fwd<64>"
     assert k("void (anonymous namespace)::stream_kernel<0, 4, 256, false>(...)") == "ceiling_copy<256>"
     assert k("void (anonymous namespace)::stream_kernel<2, 2, 64, true>(...)") == "ceiling_bwd<64,paired>"
+    assert k("void (anonymous namespace)::persist_kernel<1, 2>(...)") == "ceiling_fwd<persistent>"
     assert k("void (anonymous namespace)::bwd_kernel<2, 3>(unsigned short const*, ...)") == \
         "bwd_kernel<bf16,3>"
     assert k("void (anonymous namespace)::fwd16_kernel<2, 3, 0>(...)") == \
