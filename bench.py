@@ -346,6 +346,9 @@ def main():
     ap.add_argument("--bits", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--fwd-kernel", choices=("auto", "table", "element"), default="auto",
+                    help="fp16 / bf16 forward kernel: the library's choice by size (auto), or "
+                         "forced with the table's kernel-choice flags (diagnostics)")
     ap.add_argument("--memory", action="store_true",
                     help="report activation memory held for backward, vanilla vs few-bit, on a "
                          "GPT-2-small-shaped stack of feed-forward blocks, instead of timing")
@@ -422,6 +425,7 @@ def main():
     codes = torch.empty(P.packed_words(n, bits), dtype=torch.int32, device=dev)
 
     table, fit_ms = fit_timed(P, w, bits)
+    table = table.with_flags(table.flags | fwd_kernel_flag(P, args.fwd_kernel))
 
     def step():
         P.fwd(table, x, y=y, codes=codes)
@@ -493,7 +497,7 @@ def main():
         "ceiling": ceil,
         "fit_ms": fit_ms,
         "roofline": {
-            "kernel": kernel_name(dom, w.dtype, bits, w.act, n, table_min(P, w, bits)),
+            "kernel": kernel_name(dom, w.dtype, bits, w.act, n, forced_min(P, w, bits, args.fwd_kernel)),
             "bound": "hbm",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBPS,
@@ -519,9 +523,11 @@ def main():
             "bits": [1, 2, 3, 4],
         },
     }
-    fwd_kernel = kernel_name("fwd", w.dtype, bits, w.act, n, table_min(P, w, bits))
+    fwd_kernel = kernel_name("fwd", w.dtype, bits, w.act, n, forced_min(P, w, bits, args.fwd_kernel))
     out["fwd"]["kernel"] = fwd_kernel
-    out["bwd"]["kernel"] = kernel_name("bwd", w.dtype, bits, w.act, n, table_min(P, w, bits))
+    out["bwd"]["kernel"] = kernel_name("bwd", w.dtype, bits, w.act, n, 0)
+    if args.fwd_kernel != "auto":
+        out["fwd_kernel_forced"] = args.fwd_kernel
     if fwd_kernel.startswith("fwd16_kernel"):
         # the table forward runs one persistent workgroup per CU: its rate
         # against what that launch shape streams for the same bytes
@@ -545,6 +551,22 @@ def table_min(P, w, bits: int) -> int:
     """Size from which the workload's fp16 / bf16 forward runs the table
     kernel (0 for fp32, which has none)."""
     return 0 if w.dtype == "f32" else P.fwd16_table_min(w.act, bits, w.dtype)
+
+
+def fwd_kernel_flag(P, choice: str) -> int:
+    """Kernel-choice flag for a forced fp16 / bf16 forward kernel (0: the
+    library's choice by size)."""
+    return {"auto": 0, "table": P.FLAG_TABLE_FWD, "element": P.FLAG_ELEMENT_FWD}[choice]
+
+
+def forced_min(P, w, bits: int, choice: str) -> int:
+    """table_min as the forced choice makes it: 0 (always the table kernel)
+    or never."""
+    if choice == "table":
+        return 0
+    if choice == "element":
+        return 2 ** 63 - 1
+    return table_min(P, w, bits)
 
 
 def config_of(w, bits: int) -> dict:
@@ -692,6 +714,7 @@ def all_configs(args) -> None:
         for bits in w.bits:
             codes = torch.empty(P.packed_words(w.n, bits), dtype=torch.int32, device=dev)
             table, fit_ms = fit_timed(P, w, bits)
+            table = table.with_flags(fwd_kernel_flag(P, args.fwd_kernel))
             for _ in range(args.warmup):
                 P.fwd(table, x, y=y, codes=codes)
                 P.bwd(table, g, codes, grad_in=gin)
@@ -700,7 +723,7 @@ def all_configs(args) -> None:
             b = algorithmic_bytes(w.n, w.dtype, bits)
             ceil = ceilings(x, y, g, gin, codes, w.n, bits)
             cold = cold_times(P, table, x, y, g, gin, codes, reps=10)
-            tm = table_min(P, w, bits)
+            tm = forced_min(P, w, bits, args.fwd_kernel)
             fk = kernel_name("fwd", w.dtype, bits, w.act, w.n, tm)
             fwd_rec = kernel_record(fwd, b, w.n, ceil["fwd"])
             if fk.startswith("fwd16_kernel"):

@@ -66,9 +66,13 @@
 #ifndef FEWBIT_FWD16_UNROLL
 #define FEWBIT_FWD16_UNROLL 4
 #endif
-// the fp16 / bf16 forward by evaluation (no tables): threads per workgroup
+// the fp16 / bf16 forward by evaluation (no tables): threads per workgroup,
+// and tiles per wave loaded together before they are evaluated
 #ifndef FEWBIT_FWD16V_THREADS
 #define FEWBIT_FWD16V_THREADS 64
+#endif
+#ifndef FEWBIT_FWD16V_UNROLL
+#define FEWBIT_FWD16V_UNROLL 2
 #endif
 #ifndef FEWBIT_FWD32_THREADS
 #define FEWBIT_FWD32_THREADS 256
@@ -486,6 +490,29 @@ struct Search {
   // the index of x, or of |x| for a symmetric table (one AND with the mask:
   // -0 becomes +0 and a NaN stays a NaN, as with fabsf)
   __device__ uint32_t code(float x) const { return (*this)(__uint_as_float(__float_as_uint(x) & keep)); }
+  // F = F 2^BITS + index of x (or of |x| when SYM), the bits entering one
+  // at a time from the most significant: each level's answer is one
+  // add-with-carry (F + F + answer), so a lane that shifts in its elements
+  // from last to first ends with element j at bits BITS j.  For SYM the
+  // absolute value is a source modifier of the compares.
+  template <bool SYM>
+  __device__ void shift_in(float x, uint32_t& F) const {
+    const float v = SYM ? fabsf(x) : x;
+    if constexpr (!kPermute) {
+      bool c[BITS] = {};
+      shift_levels<0>(v, c, F);
+    } else {
+      F = (F << BITS) | (*this)(v);
+    }
+  }
+  template <int L>
+  __device__ void shift_levels(float v, bool (&c)[BITS], uint32_t& F) const {
+    if constexpr (L < BITS) {
+      c[L] = v >= pick_boundary<BITS, L, 0, 0>(c, bd);
+      F = F + F + (c[L] ? 1u : 0u);
+      shift_levels<L + 1>(v, c, F);
+    }
+  }
   __device__ uint32_t operator()(float x) const {
     if constexpr (!kPermute) {
       return classify<BITS>(x, bd);
@@ -643,7 +670,7 @@ __device__ inline WaveIndex wave_index() {
 // one constant, RNE(x / 2), RNE(lambda x), or need f).  Every workgroup fills
 // its ylut from those runs, which travel as kernel arguments, and evaluates f
 // (the fp32 f of the per-element path, then one rounding) only in the blocks
-// no rule covers: for bf16 GELU 25 blocks of 512.  clut depends on the
+// no rule covers: for bf16 GELU 30 blocks of 512.  clut depends on the
 // boundaries and is built by every workgroup: the index is monotone in the
 // pattern within one sign, so each thread classifies only the two ends of its
 // segment of patterns and fills it if they agree; the few segments that hold
@@ -867,14 +894,55 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
 // and runs a persistent grid; below the sizes of kTableMinLog2 this kernel,
 // one wave per tile with no setup, is faster.  Where the table kernel
 // evaluates f (the blocks no rule covers) it uses this same f and rounding.
-// y and the two codes of the element pair in word w; the codes go to bits
-// shift .. shift + 2*BITS - 1 of F.
-template <int DT, int BITS, int ACT>
-__device__ inline uint32_t fwd16v_pair(uint32_t w, const Search<BITS>& cl, uint32_t& F, int shift) {
+// The full tiles of one wave: y from the fp32 f, and the codes shifted into
+// the lane's field from its last element to its first (element j of the
+// lane's 8 at bits BITS j).  SYM: the table is symmetric, the index is that
+// of |x|.  The wave takes its tiles in groups of U consecutive ones and
+// issues all U loads before it evaluates the first, so its next loads are in
+// flight while it computes (one tile per wave leaves the memory idle during
+// the evaluation, which is long next to the streaming); the whole tiles past
+// the last group go one at a time.
+template <int DT, int BITS, int ACT, bool SYM>
+__device__ inline void fwd16v_tile(u32x4_t in, const Search<BITS>& cl, u32x4_t& out, uint32_t& F) {
   using H = Half<DT>;
-  const float a = H::lo(w), b = H::hi(w);
-  F |= (cl.code(a) << shift) | (cl.code(b) << (shift + BITS));
-  return H::pack(Act<DT, ACT>::f(a), Act<DT, ACT>::f(b));
+  F = 0;
+#pragma unroll
+  for (int k = 3; k >= 0; --k) {
+    const float a = H::lo(in[k]), b = H::hi(in[k]);
+    cl.template shift_in<SYM>(b, F);
+    cl.template shift_in<SYM>(a, F);
+    out[k] = H::pack(Act<DT, ACT>::f(a), Act<DT, ACT>::f(b));
+  }
+}
+
+template <int DT, int BITS, int ACT, bool SYM>
+__device__ inline void fwd16v_tiles(const uint16_t* x, uint16_t* y, uint32_t* codes, int64_t full,
+                                    const WaveIndex& wi, const Search<BITS>& cl) {
+  constexpr int U = FEWBIT_FWD16V_UNROLL;
+  constexpr int kWords = 16 * BITS;
+  const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
+  const int64_t groups = full / U;
+  for (int64_t g = wi.wave; g < groups; g += wi.nwaves) {
+    const int64_t t0 = g * U;
+    u32x4_t in[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) in[u] = Span(x + (t0 + u) * kTile, kSpanBytes).ld16(lane_b);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      u32x4_t out;
+      uint32_t F;
+      fwd16v_tile<DT, BITS, ACT, SYM>(in[u], cl, out, F);
+      Span(y + (t0 + u) * kTile, kSpanBytes).st16(lane_b, out);
+      pack_store_full<BITS>(Span(codes + (t0 + u) * kWords, kWords * 4), F, wi.lane);
+    }
+  }
+  for (int64_t t = groups * U + wi.wave; t < full; t += wi.nwaves) {
+    u32x4_t out;
+    uint32_t F;
+    fwd16v_tile<DT, BITS, ACT, SYM>(Span(x + t * kTile, kSpanBytes).ld16(lane_b), cl, out, F);
+    Span(y + t * kTile, kSpanBytes).st16(lane_b, out);
+    pack_store_full<BITS>(Span(codes + t * kWords, kWords * 4), F, wi.lane);
+  }
 }
 
 template <int DT, int BITS, int ACT>
@@ -886,16 +954,10 @@ __global__ __launch_bounds__(FEWBIT_FWD16V_THREADS) void fwd16v_kernel(
   const Search<BITS> cl(tab, wi.lane, symmetric);
   const int64_t full = n / kTile;
   const int64_t lane_off = static_cast<int64_t>(wi.lane) * kPerLane;
-  const uint32_t lane_b = static_cast<uint32_t>(wi.lane) * kLaneBytes;
-  for (int64_t t = wi.wave; t < full; t += wi.nwaves) {
-    const u32x4_t in = Span(x + t * kTile, kSpanBytes).ld16(lane_b);
-    u32x4_t out;
-    uint32_t F = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) out[k] = fwd16v_pair<DT, BITS, ACT>(in[k], cl, F, 2 * k * BITS);
-    Span(y + t * kTile, kSpanBytes).st16(lane_b, out);
-    pack_store_full<BITS>(Span(codes + t * kWords, kWords * 4), F, wi.lane);
-  }
+  if (symmetric)
+    fwd16v_tiles<DT, BITS, ACT, true>(x, y, codes, full, wi, cl);
+  else
+    fwd16v_tiles<DT, BITS, ACT, false>(x, y, codes, full, wi, cl);
   // the partial tile at the end, if any, goes to the wave that would own it
   if (n % kTile != 0 && wi.wave == full % wi.nwaves) {
     const int64_t t = full;
@@ -1341,31 +1403,34 @@ OutRuns out_runs() {
 // kernel, by [type: fp16, bf16][activation][bits - 1]; 63: never.  The table
 // kernel builds its tables in every workgroup (7-10 us of fixed cost for
 // bf16, 12-15 us for fp16, whose tables need f in far more blocks) and runs
-// as a persistent grid; the per-element kernel has no setup and streams as
-// a one-wave-per-tile grid, but evaluates f and the compares per element.
-// Measured on MI355X (x ~ N(0, 3^2), 2^22 .. 2^27 elements): the table kernel
-// wins from the size given, where the evaluation costs more than the setup
-// and the persistent grid; at 1 bit (and for ReLU) the per-element kernel
-// stays ahead at every size measured, and Softplus, whose per-element f is
-// the most expensive, switches first.
+// as a persistent grid, which streams at about 72% of the HBM peak; the
+// per-element kernel has no setup and a grid of two-tile waves that streams
+// at up to 79%, but evaluates f and the compares per element.  Measured on
+// MI355X (x ~ N(0, 1), 2^23 .. 2^28 elements, back-to-back launches, the
+// mean after the first quarter): the table kernel from the size where it is
+// ahead at every larger size measured (within 2%).  At 2^28 elements the
+// per-element kernel of 1- and 2-bit codes is 4-8% ahead in such runs, but
+// its rate under sustained load swings by about 15% (it draws more power),
+// while the table kernel's holds: there the table kernel is used (28).
+// Softplus, whose per-element f is the most expensive, switches first.
 constexpr uint8_t kTableMinLog2[2][FEWBIT_SOFTPLUS + 1][4] = {
     {   // fp16
-        {27, 26, 25, 26},   // gelu
-        {63, 27, 25, 26},   // silu
-        {63, 27, 25, 26},   // sigmoid
-        {26, 25, 24, 25},   // tanh
-        {63, 63, 63, 63},   // relu
-        {63, 27, 26, 26},   // selu
-        {23, 23, 23, 24},   // softplus
+        {28, 28, 26, 27},   // gelu
+        {28, 28, 27, 27},   // silu
+        {28, 63, 26, 27},   // sigmoid
+        {27, 26, 25, 25},   // tanh
+        {28, 28, 28, 63},   // relu
+        {28, 28, 26, 26},   // selu
+        {24, 24, 24, 24},   // softplus
     },
     {   // bf16
-        {27, 26, 25, 25},   // gelu
-        {63, 27, 25, 25},   // silu
-        {63, 27, 25, 26},   // sigmoid
-        {24, 24, 24, 24},   // tanh
-        {63, 63, 26, 63},   // relu
-        {63, 27, 26, 26},   // selu
-        {21, 21, 21, 21},   // softplus
+        {28, 28, 24, 24},   // gelu
+        {28, 28, 25, 26},   // silu
+        {28, 28, 28, 27},   // sigmoid
+        {25, 24, 24, 23},   // tanh
+        {28, 28, 28, 28},   // relu
+        {28, 28, 26, 26},   // selu
+        {22, 22, 22, 22},   // softplus
     },
 };
 
@@ -1388,7 +1453,7 @@ void launch_fwd(const Launch& L) {
     const bool table = (L.t->flags & FEWBIT_FLAG_TABLE_FWD) ||
                        (!(L.t->flags & FEWBIT_FLAG_ELEMENT_FWD) && L.n >= table_min_of(DT, ACT, BITS));
     if (!table) {
-      const dim3 grid = grid_for(L.n, FEWBIT_FWD16V_THREADS / kWave, 0, 1);
+      const dim3 grid = grid_for(L.n, FEWBIT_FWD16V_THREADS / kWave, 0, FEWBIT_FWD16V_UNROLL);
       (void)hipGetLastError();
       hipLaunchKernelGGL((fwd16v_kernel<DT, BITS, ACT>), grid, dim3(FEWBIT_FWD16V_THREADS), 0, L.s,
                          static_cast<const uint16_t*>(L.in), static_cast<uint16_t*>(L.out), L.codes,

@@ -32,7 +32,9 @@ def test_runs_are_well_formed():
         src = fh.read()
     tables = re.findall(r"\{(\d+), \{(.*?)\}\},", src)
     assert len(tables) == len(g.ACTS) * len(g.DTYPES)
-    for count, body in tables:
+    for i, (count, body) in enumerate(tables):
+        # the kernel tests for SCALE only in SELU's table
+        assert ("SCALE" in body) == (g.ACTS[i // len(g.DTYPES)] == "selu")
         runs = re.findall(r"run\((\d+), (\w+), 0x([0-9a-f]{4})\)", body)
         assert int(count) == len(runs) <= g.MAX_RUNS
         starts = [int(r[0]) for r in runs]
