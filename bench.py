@@ -227,6 +227,56 @@ def summarize_rocprof(trace_dir, fetch_dir, write_dir, workload, bits, out_traff
     print("\n".join(lines))
 
 
+SQ_DERIVED_NOTE = ("per element = x 64 lanes / elements; LDS conflict cycles per LDS "
+                   "instruction; waiting share = SQ_WAIT_ANY / SQ_WAVE_CYCLES; VALU busy = "
+                   "SQ_ACTIVE_INST_VALU / SQ_BUSY_CU_CYCLES")
+
+
+def summarize_sq(dirs, workload):
+    """Average per dispatch of the SQ counters of one or more `rocprofv3
+    --pmc` runs, per kernel, and a few ratios for the library kernels."""
+    import workloads as WL
+    w = WL.WORKLOADS[workload]
+    per = {}
+    order = []
+    for d in dirs:
+        for r in _csv(_one(d, "counter_collection.csv")):
+            key = _kernel_key(r["Kernel_Name"])
+            name = r["Counter_Name"]
+            if name not in order:
+                order.append(name)
+            per.setdefault(key, {}).setdefault(name, {}).setdefault(r["Dispatch_Id"], 0.0)
+            per[key][name][r["Dispatch_Id"]] += float(r["Counter_Value"])
+    # the library kernels, and the plain streaming copy for reference
+    keys = sorted((k for k in per if k.startswith(("fwd", "bwd")) or k == "ceiling_copy<64>"),
+                  key=lambda k: (not k.startswith(("fwd", "bwd")), k))
+    avg = {k: {c: sum(v.values()) / len(v) for c, v in per[k].items()} for k in keys}
+    lines = ["counter                  " + "".join(f"{k[:30]:>32s}" for k in keys)]
+    for c in order:
+        lines.append(f"{c:24s} " + "".join(
+            f"{avg[k][c]:32.4g}" if c in avg[k] else f"{'-':>32s}" for k in keys))
+    lines.append("")
+    lines.append(f"# derived ({SQ_DERIVED_NOTE}; {w.n:,} elements):")
+    for k in keys:
+        if not k.startswith(("fwd", "bwd")):
+            continue
+        a = avg[k]
+        parts = []
+        if "SQ_INSTS_VALU" in a:
+            parts.append(f"VALU instructions per element {a['SQ_INSTS_VALU'] * 64 / w.n:.2f}")
+        if "SQ_INSTS_LDS" in a:
+            parts.append(f"LDS instructions per element {a['SQ_INSTS_LDS'] * 64 / w.n:.2f}")
+        if "SQ_LDS_BANK_CONFLICT" in a and a.get("SQ_INSTS_LDS"):
+            parts.append(f"LDS conflict cycles per LDS instruction "
+                         f"{a['SQ_LDS_BANK_CONFLICT'] / a['SQ_INSTS_LDS']:.2f}")
+        if "SQ_WAIT_ANY" in a and a.get("SQ_WAVE_CYCLES"):
+            parts.append(f"waiting share {a['SQ_WAIT_ANY'] / a['SQ_WAVE_CYCLES']:.2f}")
+        if "SQ_ACTIVE_INST_VALU" in a and a.get("SQ_BUSY_CU_CYCLES"):
+            parts.append(f"VALU busy {a['SQ_ACTIVE_INST_VALU'] / a['SQ_BUSY_CU_CYCLES']:.2f}")
+        lines.append(f"#   {k}: " + ", ".join(parts))
+    print("\n".join(lines))
+
+
 def cpu_baseline(w, bits, x_np, g_np, seconds=10.0, chunk=1 << 22):
     """The oracle on the host: its threaded mode on the host's cores (at
     most 16, the CPU share of one GPU) over the whole input, or until
@@ -363,10 +413,15 @@ def main():
                     help="summarise a rocprofv3 --kernel-trace --stats output directory")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="calibrated HBM bytes from FETCH_SIZE and WRITE_SIZE runs")
+    ap.add_argument("--summarize-sq", nargs="+", metavar="PMC_DIR",
+                    help="print per-kernel averages of the SQ counters of rocprofv3 --pmc runs")
     ap.add_argument("--write-traffic", action="store_true",
                     help="with --summarize-counters: store profiles/traffic.json")
     args = ap.parse_args()
 
+    if args.summarize_sq:
+        summarize_sq(args.summarize_sq, args.workload)
+        return
     if args.summarize_trace or args.summarize_counters:
         fd, wd = args.summarize_counters or (None, None)
         summarize_rocprof(args.summarize_trace, fd, wd, args.workload, args.bits,

@@ -86,3 +86,34 @@ def test_kernel_keys_of_rocprof_names():
         "bwd_kernel<bf16,3>"
     assert k("void (anonymous namespace)::fwd16_kernel<2, 3, 0>(...)") == \
         "fwd16_kernel<bf16,3,gelu>"
+
+
+def test_summarize_sq_averages_per_dispatch(tmp_path, capsys):
+    # two dispatches of a library kernel (one counter split over two rows,
+    # as rocprofv3 writes per-block values) and one of a streaming kernel
+    d = tmp_path / "pmc"
+    d.mkdir()
+    rows = [
+        (1, "(anonymous namespace)::bwd_kernel<2, 3>(...)", "SQ_INSTS_VALU", 100.0e6),
+        (1, "(anonymous namespace)::bwd_kernel<2, 3>(...)", "SQ_INSTS_VALU", 60.0e6),
+        (1, "(anonymous namespace)::bwd_kernel<2, 3>(...)", "SQ_WAVE_CYCLES", 400.0),
+        (1, "(anonymous namespace)::bwd_kernel<2, 3>(...)", "SQ_WAIT_ANY", 100.0),
+        (2, "(anonymous namespace)::bwd_kernel<2, 3>(...)", "SQ_INSTS_VALU", 240.0e6),
+        (2, "(anonymous namespace)::bwd_kernel<2, 3>(...)", "SQ_WAVE_CYCLES", 400.0),
+        (2, "(anonymous namespace)::bwd_kernel<2, 3>(...)", "SQ_WAIT_ANY", 300.0),
+        (3, "void (anonymous namespace)::stream_kernel<0, 2, 64, false>(...)", "SQ_INSTS_VALU", 7.0),
+    ]
+    with open(d / "run_counter_collection.csv", "w") as fh:
+        fh.write('"Dispatch_Id","Kernel_Name","Counter_Name","Counter_Value"\n')
+        for disp, name, c, v in rows:
+            fh.write(f'{disp},"{name}","{c}",{v}\n')
+    import workloads as WL
+    w = WL.WORKLOADS["gelu3_bf16_bert_ffn_8x512x3072"]
+    bench.summarize_sq([str(d)], w.name)
+    out = capsys.readouterr().out
+    # SQ_INSTS_VALU: dispatch 1 = 160e6, dispatch 2 = 240e6 -> 200e6 per dispatch
+    assert f"VALU instructions per element {200e6 * 64 / w.n:.2f}" in out
+    assert f"{200e6 * 64 / w.n:.2f}" != f"{240e6 * 64 / w.n:.2f}"
+    # waiting share: (100/400 + 300/400) / 2 per dispatch averages -> 200 / 400
+    assert "waiting share 0.50" in out
+    assert "ceiling_copy<64>" in out
