@@ -334,7 +334,9 @@ struct Act<DT, FEWBIT_SIGMOID> {
 
 template <int DT>
 struct Act<DT, FEWBIT_TANH> {
-  __device__ static float f(float x) { return tanhf(x); }     // 16-bit tables, built once
+  // 16-bit outputs: the device libm (per element, and in the output-table
+  // blocks that no rule covers)
+  __device__ static float f(float x) { return tanhf(x); }
 };
 
 // fp32 tanh per element: 1 - 2 / (e^(2|x|) + 1) with the hardware exponential
@@ -367,7 +369,7 @@ constexpr float kSeluLambdaAlpha = 1.7580993408473766f;
 
 template <int DT>
 struct Act<DT, FEWBIT_SELU> {
-  // (the 16-bit output tables, evaluated once per device)
+  // 16-bit outputs: libm expm1f keeps the relative accuracy fp16 needs near 0
   __device__ static float f(float x) {
     return x > 0.0f ? kSeluLambda * x : kSeluLambdaAlpha * expm1f(x);   // NaN via expm1f
   }
@@ -388,7 +390,7 @@ struct Act<FEWBIT_F32, FEWBIT_SELU> {
 template <int DT>
 struct Act<DT, FEWBIT_SOFTPLUS> {
   // max(x, 0) + log(1 + e^-|x|): no overflow, full accuracy in both tails
-  // (the 16-bit output tables, evaluated once per device)
+  // (16-bit outputs: libm forms)
   __device__ static float f(float x) { return relu(x) + log1pf(expf(-fabsf(x))); }
 };
 template <>
