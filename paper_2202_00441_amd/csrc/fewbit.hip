@@ -332,20 +332,14 @@ struct Act<DT, FEWBIT_SIGMOID> {
   }
 };
 
+// tanh, every type: 1 - 2 / (e^(2|x|) + 1) with the hardware exponential and
+// reciprocal (absolute error about 2^-22, so relative error below 2^-20 where
+// |tanh| >= 0.245), and below |x| = 1/4, where that form loses relative
+// accuracy, the odd Taylor series to x^9 (first omitted term below 1e-8
+// relative), which keeps it down to the subnormals.  The sign is copied from
+// x; NaN and infinities follow from the exponential.
 template <int DT>
 struct Act<DT, FEWBIT_TANH> {
-  // 16-bit outputs: the device libm (per element, and in the output-table
-  // blocks that no rule covers)
-  __device__ static float f(float x) { return tanhf(x); }
-};
-
-// fp32 tanh per element: 1 - 2 / (e^(2|x|) + 1) with the hardware exponential
-// and reciprocal (absolute error about 2^-22), and below |x| = 1/4, where
-// that form loses relative accuracy, the odd Taylor series to x^9 (first
-// omitted term below 1e-8 relative).  The sign is copied from x; NaN and
-// infinities follow from the exponential.
-template <>
-struct Act<FEWBIT_F32, FEWBIT_TANH> {
   __device__ static float f(float x) {
     const float t = fabsf(x);
     const float e = __builtin_amdgcn_exp2f(t * (2.0f * kLog2e));
@@ -367,31 +361,55 @@ struct Act<DT, FEWBIT_RELU> {
 constexpr float kSeluLambda = 1.0507009873554805f;
 constexpr float kSeluLambdaAlpha = 1.7580993408473766f;
 
+// SELU, 16-bit outputs: lambda x, or lambda alpha (e^x - 1) for x <= 0 with
+// e^x - 1 taken from the hardware exponential from x = -1/4 down (there
+// |e^x - 1| >= 0.22, so its absolute error of ~2^-23 is a relative one below
+// 2^-20) and above -1/4 from the Taylor series to x^6 (first omitted term
+// below 6e-8 relative), which keeps relative accuracy down to the
+// subnormals.  NaN via the exponential; -inf gives -lambda alpha.
 template <int DT>
 struct Act<DT, FEWBIT_SELU> {
-  // 16-bit outputs: libm expm1f keeps the relative accuracy fp16 needs near 0
   __device__ static float f(float x) {
-    return x > 0.0f ? kSeluLambda * x : kSeluLambdaAlpha * expm1f(x);   // NaN via expm1f
+    const float e = __builtin_amdgcn_exp2f(x * kLog2e) - 1.0f;
+    const float p = x * fmaf(x, fmaf(x, fmaf(x, fmaf(x, fmaf(x, 1.0f / 720.0f, 1.0f / 120.0f), 1.0f / 24.0f),
+                                             1.0f / 6.0f), 0.5f), 1.0f);
+    const float m = x > -0.25f ? p : e;
+    return x > 0.0f ? kSeluLambda * x : kSeluLambdaAlpha * m;
   }
 };
 template <>
 struct Act<FEWBIT_F32, FEWBIT_SELU> {
   // e^x - 1 from the hardware exponential: near 0 the subtraction cancels,
   // so the error is an absolute one of about 2^-23 (times lambda alpha), not
-  // a relative one; the fp32 results stay well inside their tolerance.  The
-  // libm form above keeps the relative accuracy that fp16 outputs near 0
-  // need.  NaN via the exponential, -inf gives -lambda alpha.
+  // a relative one; the fp32 results stay well inside their tolerance (the
+  // 16-bit form above adds the series near 0 that fp16 outputs need).  NaN
+  // via the exponential, -inf gives -lambda alpha.
   __device__ static float f(float x) {
     const float e = __builtin_amdgcn_exp2f(x * kLog2e);
     return x > 0.0f ? kSeluLambda * x : kSeluLambdaAlpha * (e - 1.0f);
   }
 };
 
+// Softplus, 16-bit outputs: max(x, 0) + log(1 + u), u = e^-|x| in (0, 1]: no
+// overflow, and relative accuracy in both tails.  log(1 + u) is ln 2 log2(1 + u)
+// with the hardware log2 for u >= 2^-5 (rounding 1 + u costs at most 2^-24
+// absolute, below 2^-18 relative there) and the series u (1 - u/2 + u^2/3 -
+// u^3/4) below (first omitted term below 2^-22 relative).  The exponential is
+// taken of an argument raised by S and the series' leading factor keeps the
+// 2^S until the end, so bf16 outputs keep their relative accuracy down to
+// the subnormals (u far below 2^-126).  NaN via the exponential; +inf gives
+// +inf, -inf gives +0.
 template <int DT>
 struct Act<DT, FEWBIT_SOFTPLUS> {
-  // max(x, 0) + log(1 + e^-|x|): no overflow, full accuracy in both tails
-  // (16-bit outputs: libm forms)
-  __device__ static float f(float x) { return relu(x) + log1pf(expf(-fabsf(x))); }
+  static constexpr int S = Prec<DT>::kSigmoidS;
+  __device__ static float f(float x) {
+    const float es = __builtin_amdgcn_exp2f(fmaf(fabsf(x), -kLog2e, static_cast<float>(S)));  // 2^S u
+    constexpr float kUnscale = static_cast<float>(pow2(-S));
+    const float u = es * kUnscale;
+    const float series = (es * fmaf(u, fmaf(u, fmaf(u, -0.25f, 1.0f / 3.0f), -0.5f), 1.0f)) * kUnscale;
+    const float viaLog = __builtin_amdgcn_logf(1.0f + u) * 0.6931471805599453f;
+    return relu(x) + (u < 0x1p-5f ? series : viaLog);
+  }
 };
 template <>
 struct Act<FEWBIT_F32, FEWBIT_SOFTPLUS> {
@@ -399,7 +417,8 @@ struct Act<FEWBIT_F32, FEWBIT_SOFTPLUS> {
   // for e = e^-|x| in (0, 1].  Rounding 1 + e costs at most 2^-24 of
   // absolute error in log2, so the result is within ~2e-7 absolute of the
   // exact value (tiny outputs, x << 0, come back as absolute errors of that
-  // size, not relative ones).  The libm form above is ~3x slower.
+  // size, not relative ones, which the fp32 tolerance allows; the 16-bit
+  // form above keeps relative accuracy there).
   __device__ static float f(float x) {
     const float e = __builtin_amdgcn_exp2f(-fabsf(x) * kLog2e);
     return fmaf(__builtin_amdgcn_logf(1.0f + e), 0.6931471805599453f, relu(x));
@@ -1420,19 +1439,19 @@ constexpr uint8_t kTableMinLog2[2][FEWBIT_SOFTPLUS + 1][4] = {
         {28, 28, 26, 27},   // gelu
         {28, 28, 27, 27},   // silu
         {28, 63, 26, 27},   // sigmoid
-        {27, 26, 25, 25},   // tanh
+        {28, 27, 25, 25},   // tanh
         {28, 28, 28, 63},   // relu
-        {28, 28, 26, 26},   // selu
-        {24, 24, 24, 24},   // softplus
+        {28, 26, 25, 26},   // selu
+        {28, 28, 25, 26},   // softplus
     },
     {   // bf16
         {28, 28, 24, 24},   // gelu
         {28, 28, 25, 26},   // silu
         {28, 28, 28, 27},   // sigmoid
-        {25, 24, 24, 23},   // tanh
+        {28, 28, 24, 25},   // tanh
         {28, 28, 28, 28},   // relu
-        {28, 28, 26, 26},   // selu
-        {22, 22, 22, 22},   // softplus
+        {28, 28, 25, 27},   // selu
+        {28, 28, 24, 24},   // softplus
     },
 };
 
