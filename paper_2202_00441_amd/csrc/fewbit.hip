@@ -320,6 +320,20 @@ struct Act<DT, FEWBIT_SILU> {
   }
 };
 
+// SiLU, fp16 outputs: x sigma(x) = x / (1 + e^-x) directly.  fp16 outputs
+// below 2^-25 round to 0, long before e^-x overflows (x < -88), so the
+// negative tail needs neither the split above nor a shift; x is raised to
+// -FLT_MAX so that -inf gives -FLT_MAX * 0 = -0 (the limit), and a NaN still
+// reaches the result through the exponential.  Six instructions instead of
+// eight; every fp16 pattern within one unit in the last place.
+template <>
+struct Act<FEWBIT_F16, FEWBIT_SILU> {
+  __device__ static float f(float x) {
+    const float r = __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * -kLog2e));
+    return fmaxf(x, -3.4028234663852886e38f) * r;
+  }
+};
+
 template <int DT>
 struct Act<DT, FEWBIT_SIGMOID> {
   static constexpr int S = Prec<DT>::kSigmoidS;
