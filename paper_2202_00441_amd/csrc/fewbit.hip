@@ -20,9 +20,10 @@
 // store an identical copy, so that full tiles need no masking).
 //
 // Streams are read and written with non-temporal 16-byte buffer accesses
-// (nothing is reused).  Most kernels run one wave per tile and let the
-// hardware dispatcher balance the compute units; the table-based fp16 /
-// bf16 forward is persistent (see the launch-shape knobs below).
+// (nothing is reused).  Most kernels run one wave per tile (the per-element
+// fp16 / bf16 forward one wave per two tiles) and let the hardware
+// dispatcher balance the compute units; the table-based fp16 / bf16 forward
+// is persistent (see the launch-shape knobs below).
 //
 // fp16 / bf16 forward.  Output pattern and interval index are functions of
 // the 16-bit input pattern alone, so from a size that depends on the type,
@@ -30,8 +31,9 @@
 // LDS tables over all 65536 patterns, which it builds itself: the outputs
 // (mostly by rule, f where no rule holds) and the indices (4 bits per
 // pattern, from the boundaries).  A lookup costs two LDS reads instead of an
-// evaluation of f and the compares.  Smaller fp16 / bf16 forwards, and every
-// fp32 forward, evaluate f and search the boundaries per element.
+// evaluation of f and the compares.  Smaller fp16 / bf16 forwards (and those
+// whose f and compares are cheap enough), and every fp32 forward, evaluate f
+// and search the boundaries per element.
 //
 // The fitted table travels as kernel arguments (scalar registers); the
 // backward spreads the values over the lanes of one register and reads
@@ -927,8 +929,10 @@ __global__ __launch_bounds__(FEWBIT_FWD16_THREADS) void fwd16_kernel(
 // fp16 / bf16 forward by evaluation: f and the compares for every element,
 // no tables.  The table kernel above builds its tables in every workgroup
 // and runs a persistent grid; below the sizes of kTableMinLog2 this kernel,
-// one wave per tile with no setup, is faster.  Where the table kernel
-// evaluates f (the blocks no rule covers) it uses this same f and rounding.
+// with no setup and a dispatcher-balanced grid of two-tile waves, is
+// faster.  Where the table kernel evaluates f (the blocks no rule covers) it
+// uses this same f and rounding.
+//
 // The full tiles of one wave: y from the fp32 f, and the codes shifted into
 // the lane's field from its last element to its first (element j of the
 // lane's 8 at bits BITS j).  SYM: the table is symmetric, the index is that
