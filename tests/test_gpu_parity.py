@@ -7,10 +7,9 @@ ragged lengths, an edge-size sweep over every dtype x bits x activation,
 special values, boundaries, ReLU / SELU / Softplus (Table 1's other rows),
 both fp16 / bf16 forward kernels (per-element evaluation, and table lookups
 in tables each workgroup builds; chosen by size, or by the table's kernel
-flag),
-the symmetric (|x|) tables of Sigmoid and Tanh,
-in-place aliasing, a second stream, canaries past every output, and the
-autograd wrapper.
+flag), the symmetric (|x|) tables of Sigmoid and Tanh, in-place aliasing, a
+second stream, three streams running at once, canaries past every output,
+and the autograd wrapper.
 """
 import numpy as np
 import pytest
@@ -396,6 +395,46 @@ def test_side_stream():
     torch.cuda.synchronize()
     check_exact(download_codes(codes)[:c_ref.size], c_ref, "stream codes")
     check_y(download(y, "bf16"), y_ref, "bf16", "stream y")
+
+
+def test_concurrent_streams():
+    # The library keeps no device state: calls on three streams that run at
+    # the same time (the table forward, the per-element forward and the fp32
+    # path, with different tables, activations and bit widths, each followed
+    # by its backward, three rounds) give what each gives alone.
+    rng = np.random.default_rng(15)
+    cases = [("gelu", 3, "bf16", (1 << 22) + 1234, P.FLAG_TABLE_FWD),
+             ("silu", 2, "f16", 300001, P.FLAG_ELEMENT_FWD),
+             ("tanh", 3, "f32", 500003, 0)]
+    runs = []
+    for act, bits, dt, n, flags in cases:
+        s, v, table = _synthetic_table(act, bits)
+        table = table.with_flags(flags)
+        xb = O.round_array(ODT[dt], rng.normal(0, 2, n))
+        gb = O.round_array(ODT[dt], rng.normal(0, 1, n))
+        y_ref, c_ref = O.fwd(OACT[act], ODT[dt], bits, s, xb, threads=THREADS)
+        gin_ref = O.bwd(ODT[dt], bits, v, gb, c_ref, threads=THREADS)
+        runs.append(dict(table=table, dt=dt, x=upload(xb, dt), g=upload(gb, dt), y_ref=y_ref,
+                         c_ref=c_ref, gin_ref=gin_ref, stream=torch.cuda.Stream(), out=[]))
+    print(f"[streams] {[(c[0], c[2], c[3]) for c in cases]}", flush=True)
+    main = torch.cuda.current_stream()
+    for r in runs:
+        r["stream"].wait_stream(main)
+    for _ in range(3):
+        for r in runs:                     # interleaved launches on the three streams
+            with torch.cuda.stream(r["stream"]):
+                y, codes = P.fwd(r["table"], r["x"])
+                gin = P.bwd(r["table"], r["g"], codes)
+                r["out"].append((y, codes, gin))
+    for r in runs:
+        main.wait_stream(r["stream"])
+    torch.cuda.synchronize()
+    for r in runs:
+        for k, (y, codes, gin) in enumerate(r["out"]):
+            what = f"{r['dt']} round {k}"
+            check_exact(download_codes(codes)[:r["c_ref"].size], r["c_ref"], f"{what} codes")
+            check_y(download(y, r["dt"]), r["y_ref"], r["dt"], f"{what} y")
+            check_exact(download(gin, r["dt"]), r["gin_ref"], f"{what} grad_in")
 
 
 def _codes_at(codes_dev, idx, bits):
