@@ -1,7 +1,9 @@
 """The committed output-table rules of the 16-bit forward
 (paper_2202_00441_amd/csrc/fwd16_rules.h) are what their generator writes,
 and are well formed: per activation and type at most 16 runs, the first at
-block 0, strictly increasing starts, known rules.  The rules themselves are
+block 0, strictly increasing starts, known rules; every block a rule covers
+agrees with the oracle's forward (its own double-precision f) on all of its
+patterns, within the parity tests' 1 ulp.  The kernels that use the rules are
 checked on the GPU against the oracle over every 16-bit input pattern
 (tests/test_gpu_parity.py, test_every_input_pattern)."""
 import importlib.util
