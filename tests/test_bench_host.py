@@ -117,3 +117,19 @@ def test_summarize_sq_averages_per_dispatch(tmp_path, capsys):
     # waiting share: (100/400 + 300/400) / 2 per dispatch averages -> 200 / 400
     assert "waiting share 0.50" in out
     assert "ceiling_copy<64>" in out
+
+
+def test_forced_forward_kernel_choice():
+    # --fwd-kernel forces the 16-bit forward kernel through the table flags,
+    # and the reported kernel name follows the forced choice
+    import paper_2202_00441_amd as P
+    import workloads as WL
+    w = WL.WORKLOADS["gelu_bf16_lm_ffn_16x2048x8192"]
+    assert bench.fwd_kernel_flag(P, "auto") == 0
+    assert bench.fwd_kernel_flag(P, "table") == P.FLAG_TABLE_FWD
+    assert bench.fwd_kernel_flag(P, "element") == P.FLAG_ELEMENT_FWD
+    assert bench.forced_min(P, w, 3, "auto") == P.fwd16_table_min("gelu", 3, "bf16")
+    for choice, kernel in (("table", "fwd16_kernel"), ("element", "fwd16v_kernel")):
+        tm = bench.forced_min(P, w, 3, choice)
+        assert bench.kernel_name("fwd", "bf16", 3, "gelu", 1, tm).startswith(kernel + "<")
+        assert bench.kernel_name("fwd", "bf16", 3, "gelu", w.n, tm).startswith(kernel + "<")
